@@ -1,0 +1,272 @@
+"""Benchmark: one rank's bucketed FSDP copy path on one MI355X.
+
+A step is one pass of the whole hot path over one bucket (one transformer
+block) at rank 0:
+
+    ag_pack (fp32 shards -> bf16 chunk, written into rank 0's slot of the
+    gathered buffer), ag_unpack (gathered W*S -> full bf16 params),
+    rs_pack (full bf16 grads -> W*S send buffer), rs_reduce (W*S received
+    chunks -> fp32 grad shards).
+
+Inputs are seeded synthetic tensors of the workload's shapes and value
+distributions (params N(0, 0.02) with RMSNorm weights 1.0, grads N(0, 1e-3)
+in bf16), generated on the device before timing and resident in HBM.  The
+metric is effective HBM bandwidth: the algorithmic bytes of the step (what
+the method must read and write, padding writes included) divided by the
+step time.  Per-kernel launch durations come from HIP events recorded on the
+stream the kernels run on; the dominant kernel's figure is the roofline
+entry.  The CPU oracle is timed on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 3]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "effective HBM GB/s (and % of peak) for bucket pack/unpack/reduce"
+PEAK_GBPS = 8000.0                       # MI355X HBM3E
+KERNELS = ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")
+KERNEL_SYMBOLS = {k: f"{k}_kernel" for k in KERNELS}
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_00284_amd", "csrc", "bucket_kernels.hip")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def algorithmic_bytes(W, S, E, V0):
+    """Bytes each kernel must move (padding zero-writes included)."""
+    return {
+        "ag_pack": 4 * V0 + 2 * S,
+        "ag_unpack": 2 * E + 2 * E,
+        "rs_pack": 2 * E + 2 * W * S,
+        "rs_reduce": 2 * W * V0 + 4 * V0,
+    }
+
+
+def kernel_source_sha():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def read_traffic(kernel: str, workload: str):
+    """HBM traffic per launch from the committed counter summary, or None when
+    there is none or the kernel source changed since the counters were taken."""
+    path = os.path.join(PROFILES, f"traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
+    if not m or m.group(1) != kernel_source_sha():
+        return None
+    m = re.search(rf"^\|\s*{kernel}\s*\|[^|]*\|[^|]*\|[^|]*\|\s*([0-9.eE+]+)\s*\|", text, re.M)
+    return float(m.group(1)) if m else None
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=3, help="1 toy, 2 8B, 3 70B (default), 4 405B, 5 uneven")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="after the steps, run a plain 1 GiB device copy (for counter scaling)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
+              "the path has no collective and runs per rank", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2411_00284_amd import BucketPlan
+    from synth import workload
+
+    wl = workload(args.workload)
+    W, rank = wl.world_size, 0
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    plan = BucketPlan(W, wl.dims)
+    S = plan.chunk_elems
+    P = wl.num_params
+    E = wl.total_elems
+    V0 = sum(plan.local_elems(p, rank) for p in range(P))
+
+    # ---- seeded synthetic inputs, resident in HBM before timing
+    g = torch.Generator(device=dev)
+    g.manual_seed(1000 + args.workload)
+
+    def normal(n, scale, dtype):
+        out = torch.empty(n, dtype=dtype, device=dev)
+        step_n = 1 << 27
+        for s in range(0, n, step_n):
+            e = min(n, s + step_n)
+            out[s:e] = (torch.randn(e - s, generator=g, device=dev) * scale).to(dtype)
+        return out
+
+    shards = []
+    for p, (n, k) in enumerate(wl.dims):
+        v = plan.local_elems(p, rank)
+        shards.append(torch.ones(v, device=dev) if wl.is_norm[p] else normal(v, 0.02, torch.float32))
+    gathered = normal(W * S, 0.02, torch.bfloat16)          # the other ranks' chunks
+    send_chunk = gathered[rank * S:(rank + 1) * S]           # rank 0 packs into its own slot
+    params = [torch.empty(n * k, dtype=torch.bfloat16, device=dev) for n, k in wl.dims]
+    grads = [normal(n * k, 1e-3, torch.bfloat16) for n, k in wl.dims]
+    send_buf = torch.empty(W * S, dtype=torch.bfloat16, device=dev)
+    recv = normal(W * S, 1e-3, torch.bfloat16)
+    outs = [torch.empty(plan.local_elems(p, rank), dtype=torch.float32, device=dev) for p in range(P)]
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+
+    def run_step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        plan.ag_pack(rank, shards, send_chunk, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        plan.ag_unpack(gathered, params, stream)
+        if ev is not None:
+            ev[2].record(stream)
+        plan.rs_pack(grads, send_buf, stream)
+        if ev is not None:
+            ev[3].record(stream)
+        plan.rs_reduce(rank, recv, outs, stream)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        run_step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        run_step(events[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    per_kernel_ms = {name: [] for name in KERNELS}
+    for ev in events:
+        for i, name in enumerate(KERNELS):
+            per_kernel_ms[name].append(ev[i].elapsed_time(ev[i + 1]))
+    abytes = algorithmic_bytes(W, S, E, V0)
+    step_bytes = sum(abytes.values())
+    kernels = {}
+    for name in KERNELS:
+        avg_ms = float(np.mean(per_kernel_ms[name]))
+        gbps = abytes[name] / (avg_ms * 1e-3) / 1e9
+        kernels[name] = {"avg_us": round(avg_ms * 1e3, 2), "min_us": round(float(np.min(per_kernel_ms[name])) * 1e3, 2),
+                         "bytes": abytes[name], "GBps": round(gbps, 1), "frac": round(gbps / PEAK_GBPS, 4)}
+
+    if args.copy_probe:
+        n = 1 << 29                                # 1 GiB of bf16 read, 1 GiB written
+        a = torch.empty(n, dtype=torch.bfloat16, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    dominant = max(KERNELS, key=lambda n: kernels[n]["avg_us"])
+    dom = kernels[dominant]
+    roofline = {
+        "bound": "hbm",
+        "kernel": KERNEL_SYMBOLS[dominant],
+        "achieved": dom["GBps"],
+        "peak": PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": dom["frac"],
+        "traffic": read_traffic(dominant, wl.name),
+    }
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl)
+
+    ms_per_step = elapsed / args.steps * 1e3
+    line = {
+        "metric": METRIC,
+        "value": round(step_bytes / (elapsed / args.steps) / 1e9, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "world_size": W, "rank": rank, "params": P, "chunk_elems": S,
+                   "block_elems": E, "rank_elems": V0, "align_elems": 8, "wire": "bf16",
+                   "step": "ag_pack+ag_unpack+rs_pack+rs_reduce", "step_bytes": step_bytes},
+        "frac_of_peak": round(step_bytes / (elapsed / args.steps) / 1e9 / PEAK_GBPS, 4),
+        "kernels": kernels,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    plan.close()
+    return 0
+
+
+def cpu_baseline(wl):
+    """The oracle, as it stands, on a bounded sample of the workload: the same
+    world size and parameter shapes, restricted to the attention projections
+    and norms (wq, wk, wv, wo and both norms) when the block has them."""
+    import numpy as np
+
+    import oracle.fsdp_oracle as O
+    from synth import random_bits16, random_bits32
+
+    names = set(wl.names)
+    keep = [p for p, nm in enumerate(wl.names) if nm in ("wq", "wk", "wv", "wo", "attention_norm", "ffn_norm")]
+    if len(keep) < 2 or not {"wq", "wo"} <= names:
+        keep = list(range(wl.num_params))
+    dims = [wl.dims[p] for p in keep]
+    W = wl.world_size
+    plan = O.make_plan(W, dims, 8)
+    S = plan.chunk
+    E = sum(n * k for n, k in dims)
+    V0 = sum(O.local_elems(plan, p, 0) for p in range(len(dims)))
+    shards = [random_bits32([1, p], O.local_elems(plan, p, 0)).view(np.float32) for p in range(len(dims))]
+    shards = [np.where(np.isfinite(s), s, np.float32(0)) for s in shards]
+    gathered = random_bits16([2], W * S)
+    grads = [random_bits16([3, p], n * k).reshape(n, k) for p, (n, k) in enumerate(dims)]
+    recv = (random_bits16([4], W * S) & np.uint16(0xBFFF))      # finite: exponent MSB cleared
+    t = {}
+    t0 = time.perf_counter(); O.ag_pack(plan, 0, shards); t["ag_pack"] = time.perf_counter() - t0
+    t0 = time.perf_counter(); O.ag_unpack(plan, gathered); t["ag_unpack"] = time.perf_counter() - t0
+    t0 = time.perf_counter(); O.rs_pack(plan, grads); t["rs_pack"] = time.perf_counter() - t0
+    t0 = time.perf_counter(); O.rs_reduce(plan, 0, recv); t["rs_reduce"] = time.perf_counter() - t0
+    b = algorithmic_bytes(W, S, E, V0)
+    total_s = sum(t.values())
+    return {
+        "value": round(sum(b.values()) / total_s / 1e9, 3),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{wl.name}: params {[wl.names[p] for p in keep]} (W={W}, {E} elements, "
+                   f"{sum(b.values())} algorithmic bytes), all four steps at rank 0, numpy single thread; "
+                   f"host has {len(os.sched_getaffinity(0))} cores"),
+        "seconds": round(total_s, 3),
+        "per_kernel_s": {k: round(v, 3) for k, v in t.items()},
+    }
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,180 @@
+/*
+ * fsdp_bucket.h - one rank's share of SimpleFSDP's bucketed FSDP
+ * communication path (arXiv 2411.00284) on an AMD Instinct MI355X (gfx950).
+ *
+ * The paper makes every parameter a DTensor sharded on dim 0 over the W
+ * data-parallel ranks (section 3.1), all-gathers it to a replicated 16-bit
+ * copy before use and reduce-scatters its gradient with averaging in fp32
+ * (section 4, mixed precision and the replicate_compute listing), and groups
+ * the collectives of several parameters into one bucket: one flat buffer is
+ * filled before the collective (copy-in) and read back by each parameter's
+ * size after it (copy-out / read-out) (section 3.2.1).  This library runs
+ * the parts of that path that are local to one rank:
+ *
+ *   forward   fsdp_ag_pack    fp32 shards  -> bf16 send chunk       (copy-in)
+ *             [all-gather of the chunks: not part of this library]
+ *             fsdp_ag_unpack  gathered W chunks -> full bf16 params (copy-out)
+ *   backward  fsdp_rs_pack    full bf16 grads -> W destination chunks (copy-in)
+ *             [exchange of the chunks: not part of this library]
+ *             fsdp_rs_reduce  W received chunks -> fp32 grad shards (average + read-out)
+ *
+ * World size W is a layout parameter of the plan; no call communicates.
+ *
+ * Notation (all sizes in elements):
+ *   parameter p has shape (N_p, inner_p), row-major, inner_p = product of
+ *   the trailing dims; c_p = ceil(N_p / W) rows per rank (torch.chunk split);
+ *   rank r holds n_{p,r} = min(c_p, max(0, N_p - r*c_p)) rows;
+ *   L_p = c_p * inner_p; off_0 = 0, off_{p+1} = roundup(off_p + L_p, A);
+ *   S = roundup(off_{P-1} + L_{P-1}, A) is one rank's chunk.
+ *   Pad rows, alignment gaps and the tail of every chunk are written as +0.
+ *
+ * Conventions for every call:
+ *   - Device pointers are HIP device memory on the current device.  The
+ *     caller owns every buffer and every host pointer array; the library owns
+ *     only plans.  The hot calls allocate nothing, never synchronise, and
+ *     enqueue exactly one kernel on `stream` (0 = the null stream), or none
+ *     when there is nothing to write.
+ *   - All arguments are validated on the host before any HIP call; on any
+ *     error nothing is enqueued and no output is touched.
+ *   - Bucket buffers (send_chunk, gathered, send_buf, recv) must be 16-byte
+ *     aligned.  Per-parameter pointers need only element alignment (4 bytes
+ *     for fp32, 2 for bf16); unaligned ones take a slower element-wise path.
+ *     A per-parameter pointer may be NULL only when it has no elements.
+ *   - Outputs must not overlap inputs or each other (checked on the host).
+ *   - A plan must outlive every launch that uses it only until the call
+ *     returns (kernel arguments are copied at launch); plans are immutable
+ *     and may be shared between threads and streams.
+ *   - bf16 values are passed as uint16_t bit patterns.
+ */
+#ifndef FSDP_BUCKET_H
+#define FSDP_BUCKET_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t fsdp_status;
+
+enum {
+    FSDP_OK = 0,
+    FSDP_ERR_INVALID = 1,   /* bad argument value, NULL where data is needed, unknown plan */
+    FSDP_ERR_ALIGN = 2,     /* bucket buffer not 16-byte aligned, or element misalignment */
+    FSDP_ERR_OVERFLOW = 3,  /* a size does not fit the library's 64-bit / tile limits */
+    FSDP_ERR_TOO_MANY = 4,  /* more than FSDP_MAX_PARAMS parameters in one bucket */
+    FSDP_ERR_NOMEM = 5,     /* host allocation of a plan failed */
+    FSDP_ERR_HIP = 6,       /* the HIP runtime reported an error at launch */
+    FSDP_ERR_OVERLAP = 7    /* an output overlaps an input or another output */
+};
+
+/* Parameters per bucket: the per-parameter table travels in the kernel
+ * arguments (a Llama block has 9 parameters). */
+#define FSDP_MAX_PARAMS 64
+
+typedef struct fsdp_plan fsdp_plan;
+
+/*
+ * Plan a bucket (section 3.2.1: the bucket flattens and concatenates the
+ * parameters; section 3.1: each is sharded on dim 0 over W ranks).
+ *   world_size   W >= 1
+ *   num_params   1 <= P <= FSDP_MAX_PARAMS
+ *   dim0[P]      N_p >= 0 (host array)
+ *   inner[P]     inner_p >= 1 (host array)
+ *   align_elems  A, a power of two; 8 (16 bytes of bf16) enables the vector
+ *                path, 1 gives the dense concatenation
+ *   out          receives the plan (host memory owned by the library)
+ * Errors: FSDP_ERR_INVALID, FSDP_ERR_TOO_MANY, FSDP_ERR_OVERFLOW
+ * (N_p*inner_p, W*S or any byte size reaching 2^62, or more than 2^31-1
+ * kernel tiles), FSDP_ERR_NOMEM.  Makes no HIP call.
+ */
+fsdp_status fsdp_bucket_plan(int32_t world_size, int32_t num_params,
+                             const int64_t* dim0, const int64_t* inner,
+                             int32_t align_elems, fsdp_plan** out);
+
+/* Release a plan (NULL is ignored). */
+void fsdp_plan_free(fsdp_plan* plan);
+
+/* S, the elements of one rank's chunk; -1 for an unknown plan. */
+int64_t fsdp_plan_chunk_elems(const fsdp_plan* plan);
+
+/* W and P of a plan; -1 for an unknown plan. */
+int32_t fsdp_plan_world_size(const fsdp_plan* plan);
+int32_t fsdp_plan_num_params(const fsdp_plan* plan);
+
+/* c_p, off_p and L_p of parameter p (any output pointer may be NULL). */
+fsdp_status fsdp_plan_param(const fsdp_plan* plan, int32_t p, int64_t* rows_per_rank,
+                            int64_t* offset, int64_t* seg_elems);
+
+/* n_{p,rank}, the rows of parameter p that rank holds; -1 on a bad argument. */
+int64_t fsdp_plan_local_rows(const fsdp_plan* plan, int32_t p, int32_t rank);
+
+/* Static description of a status code. */
+const char* fsdp_status_str(fsdp_status status);
+
+/* Detail of the last failed call on this thread ("" if none). */
+const char* fsdp_last_error(void);
+
+/*
+ * Forward copy-in of rank `rank` (section 3.2.1, all-gather bucketing;
+ * section 4, parameters cast to param_dtype = bf16 before the all-gather).
+ *   shards[P]    host array of device pointers: rank's fp32 Shard(0) slab of
+ *                each parameter, n_{p,rank} x inner_p, contiguous, unpadded
+ *   send_chunk   device, S bf16 elements, 16-byte aligned; fully written:
+ *                send_chunk[off_p + k] = bf16_rne(shards[p][k]) for
+ *                k < n_{p,rank}*inner_p, +0 everywhere else
+ * The cast is IEEE round-half-to-even; a NaN becomes the quiet NaN
+ * (bits >> 16) | 0x0040 of the same sign.
+ */
+fsdp_status fsdp_ag_pack(const fsdp_plan* plan, int32_t rank,
+                         const float* const* shards, uint16_t* send_chunk,
+                         hipStream_t stream);
+
+/*
+ * Forward copy-out (section 3.2.1: gathered data copied out by each
+ * parameter's original size).
+ *   gathered     device, W*S bf16, rank-major (chunk i at gathered + i*S),
+ *                16-byte aligned; only valid rows are read
+ *   params[P]    host array of device pointers: full bf16 parameter p,
+ *                N_p x inner_p, written as
+ *                params[p][row*inner_p + col] =
+ *                  gathered[(row / c_p)*S + off_p + (row % c_p)*inner_p + col]
+ */
+fsdp_status fsdp_ag_unpack(const fsdp_plan* plan, const uint16_t* gathered,
+                           uint16_t* const* params, hipStream_t stream);
+
+/*
+ * Backward copy-in (section 3.2.1, reduce-scatter bucketing: each gradient
+ * split into W chunks, chunks concatenated per destination).
+ *   grads[P]     host array of device pointers: full bf16 gradient of
+ *                parameter p, N_p x inner_p
+ *   send_buf     device, W*S bf16, destination-major, 16-byte aligned; fully
+ *                written: send_buf[j*S + off_p + k] = grads[p][j*L_p + k] when
+ *                row j*c_p + k/inner_p < N_p, +0 otherwise (pad rows, gaps,
+ *                tail)
+ */
+fsdp_status fsdp_rs_pack(const fsdp_plan* plan, const uint16_t* const* grads,
+                         uint16_t* send_buf, hipStream_t stream);
+
+/*
+ * Rank-local average and read-out of rank `rank` (section 3.2.1: the bucket
+ * is averaged across ranks and the gradients are read out; section 4: the
+ * reduction runs in reduce_dtype = fp32; Partial("avg") -> Shard(0)).
+ *   recv         device, W*S bf16, source-major (chunk from rank i at
+ *                recv + i*S), 16-byte aligned; only valid rows are read
+ *   grad_shards[P]  host array of device pointers: fp32 output, n_{p,rank} x
+ *                inner_p each, written as
+ *                a = x_0; a = fl32(a + x_i) for i = 1..W-1; out = fl32(a / W)
+ *                with x_i = recv[i*S + off_p + k] widened exactly to fp32,
+ *                additions in rank order, a correctly rounded division and
+ *                subnormals kept.
+ */
+fsdp_status fsdp_rs_reduce(const fsdp_plan* plan, int32_t rank, const uint16_t* recv,
+                           float* const* grad_shards, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FSDP_BUCKET_H */

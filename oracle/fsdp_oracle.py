@@ -64,6 +64,10 @@ __all__ = [
     "rs_pack",
     "rs_exchange",
     "rs_reduce",
+    "ag_pack_range",
+    "ag_unpack_rows",
+    "rs_pack_range",
+    "rs_reduce_range",
 ]
 
 
@@ -292,3 +296,58 @@ def rs_reduce(plan: Plan, rank: int, recv: np.ndarray) -> list[np.ndarray]:
         res = np.divide(acc, wf, dtype=np.float32)
         out.append(res.reshape(n, k))
     return out
+
+
+# --------------------------------------------------------------------------
+# The same definitions for a slice of one output, reading only the inputs
+# that slice depends on (for buckets too large to hold several copies of on
+# the host).  ``read(...)`` callbacks return input elements as numpy arrays.
+# --------------------------------------------------------------------------
+
+def ag_pack_range(plan: Plan, rank: int, read_shard, k0: int, k1: int) -> np.ndarray:
+    """O1 restricted to send[k0:k1]; read_shard(p, lo, hi) -> fp32 shard p[lo:hi]."""
+    out = np.zeros(max(0, k1 - k0), dtype=np.uint16)
+    for p in range(plan.num_params):
+        o, v = plan.offset[p], local_elems(plan, p, rank)
+        lo, hi = max(k0, o), min(k1, o + v)
+        if lo < hi:
+            out[lo - k0:hi - k0] = bf16_rne(read_shard(p, lo - o, hi - o))
+    return out
+
+
+def ag_unpack_rows(plan: Plan, read_gathered, p: int, rows) -> np.ndarray:
+    """O3 for the listed rows of parameter p; read_gathered(start, count) ->
+    gathered[start:start+count]."""
+    k, c, o, S = plan.inner[p], plan.rows_per_rank[p], plan.offset[p], plan.chunk
+    out = np.empty((len(rows), k), dtype=np.uint16)
+    for t, row in enumerate(rows):
+        if not 0 <= row < plan.rows[p]:
+            raise ValueError("row out of range")
+        i, q = divmod(int(row), c)
+        out[t] = read_gathered(i * S + o + q * k, k)
+    return out
+
+
+def rs_pack_range(plan: Plan, read_grad, j: int, k0: int, k1: int) -> np.ndarray:
+    """O4 restricted to send[j*S + k0 : j*S + k1]; read_grad(p, lo, hi) ->
+    flattened bf16 gradient p[lo:hi]."""
+    out = np.zeros(max(0, k1 - k0), dtype=np.uint16)
+    for p in range(plan.num_params):
+        o, L, k = plan.offset[p], plan.seg[p], plan.inner[p]
+        valid = local_rows(plan, p, j) * k          # rows j*c .. that exist
+        lo, hi = max(k0, o), min(k1, o + min(L, valid))
+        if lo < hi:
+            out[lo - k0:hi - k0] = read_grad(p, j * L + (lo - o), j * L + (hi - o))
+    return out
+
+
+def rs_reduce_range(plan: Plan, rank: int, read_recv, p: int, e0: int, e1: int) -> np.ndarray:
+    """O6 for elements [e0, e1) of parameter p's output shard; read_recv(start,
+    count) -> recv[start:start+count]."""
+    W, S, o = plan.world_size, plan.chunk, plan.offset[p]
+    if not 0 <= e0 <= e1 <= local_elems(plan, p, rank):
+        raise ValueError("range outside the shard")
+    acc = bf16_to_f32(read_recv(o + e0, e1 - e0))
+    for i in range(1, W):
+        acc = np.add(acc, bf16_to_f32(read_recv(i * S + o + e0, e1 - e0)), dtype=np.float32)
+    return np.divide(acc, np.float32(W), dtype=np.float32)

@@ -1,0 +1,48 @@
+// Internal view of a bucket plan, shared by the planner and the launchers.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "fsdp_bucket.h"
+
+namespace fsdp {
+
+// Output elements handled by one work tile of the copy kernels and of the
+// reduction (a 256-thread workgroup, 8 elements = 16 bytes per thread and
+// step; the copy kernels take 4 steps per tile, the reduction 1).
+constexpr int kBlock = 256;
+constexpr int kVec = 8;
+constexpr int64_t kCopyTile = int64_t(kBlock) * kVec * 4;
+constexpr int64_t kReduceTile = int64_t(kBlock) * kVec;
+
+struct Plan {
+    int32_t world;     // W
+    int32_t nparams;   // P
+    int32_t align;     // A (elements)
+    int64_t chunk;     // S
+    std::vector<int64_t> rows;     // N_p
+    std::vector<int64_t> inner;    // inner_p
+    std::vector<int64_t> cpr;      // c_p
+    std::vector<int64_t> seg;      // L_p
+    std::vector<int64_t> off;      // off_p, with off[P] = S
+    std::vector<int64_t> elems;    // N_p * inner_p
+
+    int64_t local_rows(int p, int r) const {
+        int64_t c = cpr[p];
+        int64_t rest = rows[p] - int64_t(r) * c;
+        return rest <= 0 ? 0 : (rest < c ? rest : c);
+    }
+    int64_t local_elems(int p, int r) const { return local_rows(p, r) * inner[p]; }
+};
+
+// Plans handed out by fsdp_bucket_plan and not yet freed.
+bool plan_is_live(const fsdp_plan* h);
+const Plan* plan_of(const fsdp_plan* h);
+
+// Thread-local detail for fsdp_last_error.
+fsdp_status fail(fsdp_status s, const std::string& msg);
+void clear_error();
+
+}  // namespace fsdp

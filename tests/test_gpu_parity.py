@@ -1,0 +1,362 @@
+"""GPU parity: every kernel, through the C ABI, against the CPU oracle, bit for bit.
+
+Outputs live inside poisoned guard bands: every output element must equal the
+oracle's (so nothing is left unwritten) and the guards must be intact (so
+nothing is written out of bounds).  Small buckets cover the edge cases (empty
+parameters, ranks holding no rows, W = 1, dim 0 smaller than W, 1-wide
+parameters, the dense align = 1 layout, element-aligned parameter pointers,
+the parameter limit, several tiles with ragged tails); the Llama-shaped
+workloads run at full size in the launch configuration the benchmark times.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.fsdp_oracle as O
+from gpu_util import (DEV, Guarded, dev_random_bits16, dev_random_f32_bits, dev_wide_bf16, host_u16,
+                      host_u32, step, to_dev_f32, to_dev_u16)
+from synth import WORKLOADS, random_bits16, random_bits32
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+if torch.cuda.is_available():
+    from paper_2411_00284_amd import BucketPlan
+
+
+SMALL = [
+    (1, [(5, 3), (1, 1), (0, 4)]),
+    (2, [(5, 3), (1, 1), (7, 2), (0, 4)]),
+    (3, [(7, 3), (2, 5), (10, 1), (3, 8)]),
+    (4, [(16, 8), (9, 3), (3, 1), (4, 16), (1, 7)]),
+    (7, [(20, 2), (6, 1), (13, 9)]),
+    (8, [(17, 8), (8, 8), (64, 1), (1, 1)]),
+    (48, [(86, 1), (4096, 1), (1, 3), (47, 2), (49, 1)]),
+    (64, [(65, 1), (128, 2), (0, 3)]),
+    # several tiles per segment, ragged tails, unaligned segment lengths
+    (3, [(5000, 7), (4096, 4), (1, 1), (20000, 1), (2049, 8)]),
+    (5, [(40000, 3), (9, 4096)]),
+    # the parameter limit
+    (4, [(i % 13, 1 + i % 5) for i in range(64)]),
+]
+
+
+def _ranks(w):
+    return sorted({0, w // 2, w - 1})
+
+
+# ----------------------------------------------------------------- one kernel each
+
+def run_ag_pack(plan, oplan, rank, seed, shift=0):
+    """Random fp32 bit patterns (NaN, inf, subnormals) as the rank's shards."""
+    P = oplan.num_params
+    host = [random_bits32([seed, rank, p], O.local_elems(oplan, p, rank)).view(np.float32) for p in range(P)]
+    bufs = [Guarded(h.size, torch.float32, shift) for h in host]
+    for b, h in zip(bufs, host):
+        if h.size:
+            b.view.copy_(to_dev_f32(h))
+    out = Guarded(oplan.chunk, torch.bfloat16)
+    step(f"ag_pack W={oplan.world_size} P={P} rank={rank} align={oplan.align} shift={shift}")
+    plan.ag_pack(rank, [b.view for b in bufs], out.view)
+    torch.cuda.synchronize()
+    assert out.guards_intact()
+    assert np.array_equal(host_u16(out.view), O.ag_pack(oplan, rank, host))
+
+
+def run_ag_unpack(plan, oplan, seed, shift=0):
+    W, S = oplan.world_size, oplan.chunk
+    g = random_bits16([seed, 1], W * S)
+    gathered = Guarded(W * S, torch.bfloat16)
+    gathered.view.copy_(to_dev_u16(g))
+    outs = [Guarded(n * k, torch.bfloat16, shift) for n, k in zip(oplan.rows, oplan.inner)]
+    step(f"ag_unpack W={W} P={oplan.num_params} align={oplan.align} shift={shift}")
+    plan.ag_unpack(gathered.view, [o.view for o in outs])
+    torch.cuda.synchronize()
+    want = O.ag_unpack(oplan, g)
+    for p, o in enumerate(outs):
+        assert o.guards_intact(), p
+        assert np.array_equal(host_u16(o.view), want[p].reshape(-1)), p
+    assert np.array_equal(host_u16(gathered.view), g)           # input untouched
+
+
+def run_rs_pack(plan, oplan, seed, shift=0):
+    W, S = oplan.world_size, oplan.chunk
+    grads = [random_bits16([seed, 2, p], n * k) for p, (n, k) in enumerate(zip(oplan.rows, oplan.inner))]
+    bufs = [Guarded(g.size, torch.bfloat16, shift) for g in grads]
+    for b, g in zip(bufs, grads):
+        if g.size:
+            b.view.copy_(to_dev_u16(g))
+    out = Guarded(W * S, torch.bfloat16)
+    step(f"rs_pack W={W} P={oplan.num_params} align={oplan.align} shift={shift}")
+    plan.rs_pack([b.view for b in bufs], out.view)
+    torch.cuda.synchronize()
+    assert out.guards_intact()
+    want = O.rs_pack(oplan, [g.reshape(n, k) for g, n, k in zip(grads, oplan.rows, oplan.inner)])
+    assert np.array_equal(host_u16(out.view), want)
+
+
+def run_rs_reduce(plan, oplan, rank, recv_host, shift=0):
+    W, S = oplan.world_size, oplan.chunk
+    recv = Guarded(W * S, torch.bfloat16)
+    recv.view.copy_(to_dev_u16(recv_host))
+    outs = [Guarded(O.local_elems(oplan, p, rank), torch.float32, shift) for p in range(oplan.num_params)]
+    step(f"rs_reduce W={W} P={oplan.num_params} rank={rank} align={oplan.align} shift={shift}")
+    plan.rs_reduce(rank, recv.view, [o.view for o in outs])
+    torch.cuda.synchronize()
+    want = O.rs_reduce(oplan, rank, recv_host)
+    for p, o in enumerate(outs):
+        assert o.guards_intact(), p
+        assert np.array_equal(host_u32(o.view), want[p].reshape(-1).view(np.uint32)), p
+
+
+def wide_bf16_host(words, n):
+    """Finite bf16 values over a wide exponent range (host copy of the same recipe)."""
+    rng = np.random.default_rng(words)
+    g = rng.standard_normal(n) * np.exp2(rng.integers(-20, 21, n))
+    return (g.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+# ----------------------------------------------------------------- small buckets
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+@pytest.mark.parametrize("align", [8, 1])
+def test_small_buckets(case, align):
+    w, dims = SMALL[case]
+    plan = BucketPlan(w, dims, align)
+    oplan = O.make_plan(w, dims, align)
+    assert plan.chunk_elems == oplan.chunk
+    for shift in (0, 1):
+        for r in _ranks(w):
+            run_ag_pack(plan, oplan, r, seed=case, shift=shift)
+        run_ag_unpack(plan, oplan, seed=case, shift=shift)
+        run_rs_pack(plan, oplan, seed=case, shift=shift)
+        recv = wide_bf16_host([case, align], w * oplan.chunk)
+        for r in _ranks(w):
+            run_rs_reduce(plan, oplan, r, recv, shift=shift)
+    plan.close()
+
+
+def test_reduce_special_values():
+    """Signed zeros, infinities, NaN and subnormals through the reduction."""
+    w = 3
+    dims = [(w * 40, 8)]
+    plan = BucketPlan(w, dims)
+    oplan = O.make_plan(w, dims)
+    S = oplan.chunk
+    specials = np.array([0x0000, 0x8000, 0x7F80, 0xFF80, 0x7FC0, 0x0001, 0x8001, 0x007F, 0x0080,
+                         0x3F80, 0xBF80, 0x7F7F, 0xFF7F], np.uint16)
+    rng = np.random.default_rng(5)
+    recv = specials[rng.integers(0, specials.size, w * S)]
+    recv[:S] = 0x8000                   # first rows: every source -0 -> -0
+    recv[S:2 * S][:64] = 0x8000
+    recv[2 * S:3 * S][:64] = 0x8000
+    for r in range(w):
+        run_rs_reduce(plan, oplan, r, recv)
+
+
+def test_pack_special_values():
+    """The fp32 -> bf16 cast on the hand-worked table and on every NaN class."""
+    cases = [0x3F800000, 0x3F808000, 0x3F818000, 0x3F808001, 0x3F807FFF, 0x3F80FFFF, 0x3FFF8000,
+             0x7F7FFFFF, 0x7F7F7FFF, 0x7F7F8000, 0x7F800000, 0xFF800000, 0x80000000, 0x00000000,
+             0x00000001, 0x00008000, 0x00018000, 0x007FFFFF, 0x00400000, 0xBF808000, 0xBF818000,
+             0x7FC00000, 0xFFC00000, 0x7F800001, 0xFF800001, 0x7FFFFFFF, 0xFFFFFFFF]
+    x = np.array(cases * 40, np.uint32).view(np.float32)
+    dims = [(x.size, 1)]
+    plan = BucketPlan(1, dims)
+    oplan = O.make_plan(1, dims)
+    out = Guarded(oplan.chunk, torch.bfloat16)
+    step("ag_pack special values")
+    plan.ag_pack(0, [to_dev_f32(x)], out.view)
+    torch.cuda.synchronize()
+    assert out.guards_intact()
+    assert np.array_equal(host_u16(out.view), O.ag_pack(oplan, 0, [x]))
+
+
+def test_non_default_stream():
+    w, dims = 4, [(300, 64), (7, 3)]
+    plan = BucketPlan(w, dims)
+    oplan = O.make_plan(w, dims)
+    S = oplan.chunk
+    g = random_bits16([77], w * S)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        gathered = to_dev_u16(g)
+        outs = [torch.empty(n * k, dtype=torch.bfloat16, device=DEV) for n, k in dims]
+        step("ag_unpack on a side stream")
+        plan.ag_unpack(gathered, outs)            # enqueued on the current (side) stream
+    s.synchronize()
+    want = O.ag_unpack(oplan, g)
+    for p in range(len(dims)):
+        assert np.array_equal(host_u16(outs[p]), want[p].reshape(-1))
+
+
+def test_repeat_calls_are_identical():
+    """Poisoned outputs, two calls in a row: the second overwrites exactly as the first."""
+    w, dims = 8, [(1000, 24), (33, 1)]
+    plan = BucketPlan(w, dims)
+    oplan = O.make_plan(w, dims)
+    for _ in range(2):
+        run_rs_pack(plan, oplan, seed=3)
+        run_ag_pack(plan, oplan, 7, seed=3)
+
+
+# ----------------------------------------------------------------- full-size workloads
+
+def _full_ag_pack(plan, oplan, rank, seed):
+    P = oplan.num_params
+    shards = [dev_random_f32_bits(O.local_elems(oplan, p, rank), seed * 1000 + p) for p in range(P)]
+    out = Guarded(oplan.chunk, torch.bfloat16)
+    step(f"ag_pack full W={oplan.world_size} rank={rank}")
+    plan.ag_pack(rank, shards, out.view)
+    torch.cuda.synchronize()
+    assert out.guards_intact()
+    host = [host_u32(s).view(np.float32) for s in shards]
+    assert np.array_equal(host_u16(out.view), O.ag_pack(oplan, rank, host))
+
+
+def _full_ag_unpack(plan, oplan, seed):
+    W, S = oplan.world_size, oplan.chunk
+    gathered = dev_random_bits16(W * S, seed)
+    outs = [Guarded(n * k, torch.bfloat16) for n, k in zip(oplan.rows, oplan.inner)]
+    step(f"ag_unpack full W={W}")
+    plan.ag_unpack(gathered, [o.view for o in outs])
+    torch.cuda.synchronize()
+    g = host_u16(gathered)
+    want = O.ag_unpack(oplan, g)
+    del g
+    for p, o in enumerate(outs):
+        assert o.guards_intact(), p
+        assert np.array_equal(host_u16(o.view), want[p].reshape(-1)), p
+
+
+def _full_rs_pack(plan, oplan, seed):
+    W, S = oplan.world_size, oplan.chunk
+    grads = [dev_random_bits16(n * k, seed * 100 + p) for p, (n, k) in enumerate(zip(oplan.rows, oplan.inner))]
+    out = Guarded(W * S, torch.bfloat16)
+    step(f"rs_pack full W={W}")
+    plan.rs_pack(grads, out.view)
+    torch.cuda.synchronize()
+    assert out.guards_intact()
+    host = [host_u16(g).reshape(n, k) for g, n, k in zip(grads, oplan.rows, oplan.inner)]
+    del grads
+    assert np.array_equal(host_u16(out.view), O.rs_pack(oplan, host))
+
+
+def _full_rs_reduce(plan, oplan, rank, seed):
+    W, S = oplan.world_size, oplan.chunk
+    recv = dev_wide_bf16(W * S, seed)
+    outs = [Guarded(O.local_elems(oplan, p, rank), torch.float32) for p in range(oplan.num_params)]
+    step(f"rs_reduce full W={W} rank={rank}")
+    plan.rs_reduce(rank, recv, [o.view for o in outs])
+    torch.cuda.synchronize()
+    want = O.rs_reduce(oplan, rank, host_u16(recv))
+    for p, o in enumerate(outs):
+        assert o.guards_intact(), p
+        assert np.array_equal(host_u32(o.view), want[p].reshape(-1).view(np.uint32)), p
+
+
+@pytest.mark.parametrize("key", [1, 2, 3, 5])
+@pytest.mark.parametrize("kernel", ["ag_pack", "ag_unpack", "rs_pack", "rs_reduce"])
+def test_workload_full(key, kernel):
+    wl = WORKLOADS[key]
+    plan = BucketPlan(wl.world_size, wl.dims)
+    oplan = O.make_plan(wl.world_size, wl.dims)
+    W = wl.world_size
+    if kernel == "ag_pack":
+        for r in _ranks(W):
+            _full_ag_pack(plan, oplan, r, seed=key)
+    elif kernel == "ag_unpack":
+        _full_ag_unpack(plan, oplan, seed=key)
+    elif kernel == "rs_pack":
+        _full_rs_pack(plan, oplan, seed=key)
+    else:
+        for r in sorted({0, W - 1}):
+            _full_rs_reduce(plan, oplan, r, seed=key * 10 + r)
+    plan.close()
+    torch.cuda.empty_cache()
+
+
+# ----------------------------------------------------------------- the 405B block, sampled
+
+def _reader(t):
+    return lambda start, count: host_u16(t[start:start + count])
+
+
+def test_workload_405b_sampled():
+    """405B block, W = 128 (W*S = 3.19e9 elements: 64-bit indexing).  ag_pack and
+    rs_reduce outputs are compared in full; ag_unpack and rs_pack outputs (6.4 GB
+    each) on sampled rows and ranges that include every rank-segment and
+    parameter boundary of the sampled ranks."""
+    wl = WORKLOADS[4]
+    W = wl.world_size
+    plan = BucketPlan(W, wl.dims)
+    oplan = O.make_plan(W, wl.dims)
+    S = oplan.chunk
+    assert W * S > 2 ** 31
+    _full_ag_pack(plan, oplan, W - 1, seed=4)
+
+    rng = np.random.default_rng(405)
+    gathered = dev_random_bits16(W * S, 41)
+    outs = [torch.empty(n * k, dtype=torch.bfloat16, device=DEV) for n, k in wl.dims]
+    step("ag_unpack 405B")
+    plan.ag_unpack(gathered, outs)
+    torch.cuda.synchronize()
+    read = _reader(gathered)
+    for p, (n, k) in enumerate(wl.dims):
+        c = oplan.rows_per_rank[p]
+        rows = {0, n - 1}
+        for i in (0, 1, W // 2, W - 2, W - 1):
+            rows |= {min(n - 1, i * c), min(n - 1, i * c + c - 1)}
+        rows |= set(int(x) for x in rng.integers(0, n, 16))
+        rows = sorted(rows)
+        want = O.ag_unpack_rows(oplan, read, p, rows)
+        got = outs[p].view(n, k)[torch.tensor(rows, device=DEV)]
+        assert np.array_equal(host_u16(got).reshape(len(rows), k), want), p
+    del gathered, outs
+    torch.cuda.empty_cache()
+
+    grads = [dev_random_bits16(n * k, 4100 + p) for p, (n, k) in enumerate(wl.dims)]
+    send = Guarded(W * S, torch.bfloat16)
+    step("rs_pack 405B")
+    plan.rs_pack(grads, send.view)
+    torch.cuda.synchronize()
+    assert send.guards_intact()
+
+    def read_grad(p, lo, hi):
+        return host_u16(grads[p][lo:hi])
+
+    for j in (0, 1, W // 2, W - 1):
+        bounds = [0, S]
+        for p in range(oplan.num_params):
+            bounds += [oplan.offset[p], oplan.offset[p] + oplan.seg[p]]
+        for b in sorted(set(bounds)):
+            k0, k1 = max(0, b - 2048), min(S, b + 2048)
+            got = host_u16(send.view[j * S + k0:j * S + k1])
+            assert np.array_equal(got, O.rs_pack_range(oplan, read_grad, j, k0, k1)), (j, b)
+        for k0 in rng.integers(0, S - 65536, 4):
+            k0 = int(k0)
+            got = host_u16(send.view[j * S + k0:j * S + k0 + 65536])
+            assert np.array_equal(got, O.rs_pack_range(oplan, read_grad, j, k0, k0 + 65536)), (j, k0)
+    del grads, send
+    torch.cuda.empty_cache()
+
+    for r in (0, W - 1):
+        recv = dev_wide_bf16(W * S, 4200 + r)
+        outs = [torch.empty(O.local_elems(oplan, p, r), dtype=torch.float32, device=DEV)
+                for p in range(oplan.num_params)]
+        step(f"rs_reduce 405B rank={r}")
+        plan.rs_reduce(r, recv, outs)
+        torch.cuda.synchronize()
+        rd = _reader(recv)
+        for p in range(oplan.num_params):
+            v = O.local_elems(oplan, p, r)
+            for e0 in sorted({0, max(0, v - 4096)} | set(int(x) for x in rng.integers(0, max(1, v - 4096), 3))):
+                e1 = min(v, e0 + 4096)
+                want = O.rs_reduce_range(oplan, r, rd, p, e0, e1)
+                assert np.array_equal(host_u32(outs[p][e0:e1]), want.view(np.uint32)), (r, p, e0)
+        del recv, outs
+        torch.cuda.empty_cache()
+    plan.close()

@@ -225,3 +225,44 @@ def test_pins_catch_mutant(name):
         impl.make_plan = mp
     with pytest.raises((AssertionError, ValueError)):
         run_all_checks(impl, quick=True)
+
+
+# ----------------------------------------------------------------- sliced forms
+
+@pytest.mark.parametrize("w,dims", SMALL_CASES[:6] + [(48, [(86, 1), (100, 3), (1, 8)])])
+def test_sliced_forms_equal_full_forms(w, dims):
+    """The sliced oracle entry points (used at full bucket sizes) agree with the
+    full-buffer ones on every slice of small buckets."""
+    from synth import random_bits16, random_bits32
+    for align in (8, 1):
+        plan = O.make_plan(w, dims, align)
+        S = plan.chunk
+        rng = np.random.default_rng(w)
+        for r in sorted({0, w // 2, w - 1}):
+            shards = [random_bits32([w, r, p], O.local_elems(plan, p, r)).view(np.float32)
+                      for p in range(len(dims))]
+            full = O.ag_pack(plan, r, shards)
+            for _ in range(5):
+                k0 = int(rng.integers(0, S + 1)); k1 = int(rng.integers(k0, S + 1))
+                got = O.ag_pack_range(plan, r, lambda p, lo, hi: shards[p][lo:hi], k0, k1)
+                assert np.array_equal(got, full[k0:k1])
+        g = random_bits16([w, 7], w * S)
+        unp = O.ag_unpack(plan, g)
+        for p, (n, k) in enumerate(dims):
+            rows = list(range(n))
+            assert np.array_equal(O.ag_unpack_rows(plan, lambda s, c: g[s:s + c], p, rows), unp[p])
+        grads = [random_bits16([w, 8, p], n * k).reshape(n, k) for p, (n, k) in enumerate(dims)]
+        send = O.rs_pack(plan, grads)
+        for j in range(w):
+            for k0, k1 in ((0, S), (1, S - 1), (S // 3, S // 2)):
+                if k0 > k1:
+                    continue
+                got = O.rs_pack_range(plan, lambda p, lo, hi: grads[p].reshape(-1)[lo:hi], j, k0, k1)
+                assert np.array_equal(got, send[j * S + k0:j * S + k1])
+        recv = random_bits16([w, 9], w * S)
+        for r in sorted({0, w - 1}):
+            red = O.rs_reduce(plan, r, recv)
+            for p in range(len(dims)):
+                v = O.local_elems(plan, p, r)
+                got = O.rs_reduce_range(plan, r, lambda s, c: recv[s:s + c], p, 0, v)
+                assert np.array_equal(got.view(np.uint32), red[p].reshape(-1).view(np.uint32))
