@@ -34,10 +34,22 @@
 namespace fsdp {
 namespace {
 
+#ifndef FSDP_REDUCE_BATCH
+#define FSDP_REDUCE_BATCH 4
+#endif
+#ifndef FSDP_BLOCKS_PER_CU
+#define FSDP_BLOCKS_PER_CU 4096
+#endif
+#ifndef FSDP_NT_LOAD
+#define FSDP_NT_LOAD 1
+#endif
+#ifndef FSDP_NT_STORE
+#define FSDP_NT_STORE 1
+#endif
+
 constexpr int PMAX = FSDP_MAX_PARAMS;
-constexpr int kCopySteps = int(kCopyTile / (int64_t(kBlock) * kVec));   // 4
-constexpr int kReduceBatch = 8;        // source ranks loaded before they are added
-constexpr int kBlocksPerCU = 8;        // workgroups per CU in the grid-stride launch
+constexpr int kReduceBatch = FSDP_REDUCE_BATCH;   // source ranks loaded before they are added
+constexpr int kBlocksPerCU = FSDP_BLOCKS_PER_CU;  // workgroups per CU in the grid-stride launch
 
 // ------------------------------------------------------------------ device helpers
 
@@ -61,8 +73,46 @@ __device__ __forceinline__ int param_of_tile(int my_start, int t) {
     return __builtin_amdgcn_readfirstlane(__popcll(m) - 1);
 }
 
-__device__ __forceinline__ uint4 ld16(const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); }
-__device__ __forceinline__ void st16(uint16_t* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte accesses; streamed data may bypass cache retention (non-temporal).
+__device__ __forceinline__ uint4 ld16(const uint16_t* p) {
+    const u32x4* q = reinterpret_cast<const u32x4*>(p);
+#if FSDP_NT_LOAD
+    const u32x4 v = __builtin_nontemporal_load(q);
+#else
+    const u32x4 v = *q;
+#endif
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void st16(uint16_t* p, uint4 v) {
+    u32x4* q = reinterpret_cast<u32x4*>(p);
+    const u32x4 w = {v.x, v.y, v.z, v.w};
+#if FSDP_NT_STORE
+    __builtin_nontemporal_store(w, q);
+#else
+    *q = w;
+#endif
+}
+__device__ __forceinline__ float4 ldf16(const float* p) {
+    const f32x4* q = reinterpret_cast<const f32x4*>(p);
+#if FSDP_NT_LOAD
+    const f32x4 v = __builtin_nontemporal_load(q);
+#else
+    const f32x4 v = *q;
+#endif
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void stf16(float* p, float4 v) {
+    f32x4* q = reinterpret_cast<f32x4*>(p);
+    const f32x4 w = {v.x, v.y, v.z, v.w};
+#if FSDP_NT_STORE
+    __builtin_nontemporal_store(w, q);
+#else
+    *q = w;
+#endif
+}
 
 // ------------------------------------------------------------------ ag_pack
 
@@ -78,13 +128,13 @@ struct PackArgs {
 };
 
 __device__ __forceinline__ uint4 cast8(const float* __restrict__ s) {
-    const float4 a = *reinterpret_cast<const float4*>(s);
-    const float4 b = *reinterpret_cast<const float4*>(s + 4);
+    const float4 a = ldf16(s);
+    const float4 b = ldf16(s + 4);
     return make_uint4(bf16x2_bits(a.x, a.y), bf16x2_bits(a.z, a.w),
                       bf16x2_bits(b.x, b.y), bf16x2_bits(b.z, b.w));
 }
 
-__global__ void __launch_bounds__(kBlock) ag_pack_kernel(const PackArgs a) {
+__global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
@@ -101,14 +151,14 @@ __global__ void __launch_bounds__(kBlock) ag_pack_kernel(const PackArgs a) {
             uint4 v[kCopySteps];
 #pragma unroll
             for (int u = 0; u < kCopySteps; ++u)
-                v[u] = cast8(src + lo + (int64_t(u) * kBlock + threadIdx.x) * kVec);
+                v[u] = cast8(src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec);
 #pragma unroll
             for (int u = 0; u < kCopySteps; ++u)
-                st16(dst + lo + (int64_t(u) * kBlock + threadIdx.x) * kVec, v[u]);
+                st16(dst + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec, v[u]);
             continue;
         }
         for (int u = 0; u < kCopySteps; ++u) {
-            const int64_t g = lo + (int64_t(u) * kBlock + threadIdx.x) * kVec;
+            const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
             if (g >= hi) break;
             if (vec && g + kVec <= hi && (g + kVec <= valid || g >= valid)) {
                 st16(dst + g, g < valid ? cast8(src + g) : make_uint4(0, 0, 0, 0));
@@ -144,13 +194,13 @@ __device__ __forceinline__ void copy_range(const uint16_t* __restrict__ s, uint1
     if (vec && hi - lo == kCopyTile) {
         uint4 v[kCopySteps];
 #pragma unroll
-        for (int u = 0; u < kCopySteps; ++u) v[u] = ld16(s + lo + (int64_t(u) * kBlock + threadIdx.x) * kVec);
+        for (int u = 0; u < kCopySteps; ++u) v[u] = ld16(s + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec);
 #pragma unroll
-        for (int u = 0; u < kCopySteps; ++u) st16(d + lo + (int64_t(u) * kBlock + threadIdx.x) * kVec, v[u]);
+        for (int u = 0; u < kCopySteps; ++u) st16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec, v[u]);
         return;
     }
     for (int u = 0; u < kCopySteps; ++u) {
-        const int64_t g = lo + (int64_t(u) * kBlock + threadIdx.x) * kVec;
+        const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
         if (g >= hi) break;
         if (vec && g + kVec <= hi) {
             st16(d + g, ld16(s + g));
@@ -161,7 +211,7 @@ __device__ __forceinline__ void copy_range(const uint16_t* __restrict__ s, uint1
     }
 }
 
-__global__ void __launch_bounds__(kBlock) ag_unpack_kernel(const UnpackArgs a) {
+__global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
@@ -199,7 +249,7 @@ struct RsPackArgs {
     int32_t ntiles;
 };
 
-__global__ void __launch_bounds__(kBlock) rs_pack_kernel(const RsPackArgs a) {
+__global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
@@ -225,12 +275,12 @@ __global__ void __launch_bounds__(kBlock) rs_pack_kernel(const RsPackArgs a) {
             } else {
 #pragma unroll
                 for (int u = 0; u < kCopySteps; ++u)
-                    st16(d + lo + (int64_t(u) * kBlock + threadIdx.x) * kVec, make_uint4(0, 0, 0, 0));
+                    st16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec, make_uint4(0, 0, 0, 0));
             }
             continue;
         }
         for (int u = 0; u < kCopySteps; ++u) {
-            const int64_t g = lo + (int64_t(u) * kBlock + threadIdx.x) * kVec;
+            const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
             if (g >= hi) break;
             if (vec && g + kVec <= hi && (g + kVec <= v || g >= v)) {
                 st16(d + g, g < v ? ld16(s + g) : make_uint4(0, 0, 0, 0));
@@ -266,7 +316,76 @@ __device__ __forceinline__ void add8(float (&acc)[8], uint4 x) {
     acc[6] += bf16_lo(x.w); acc[7] += bf16_hi(x.w);
 }
 
-__global__ void __launch_bounds__(kBlock) rs_reduce_kernel(const ReduceArgs a) {
+__device__ __forceinline__ void init8(float (&acc)[8], uint4 x) {
+    acc[0] = bf16_lo(x.x); acc[1] = bf16_hi(x.x);
+    acc[2] = bf16_lo(x.y); acc[3] = bf16_hi(x.y);
+    acc[4] = bf16_lo(x.z); acc[5] = bf16_hi(x.z);
+    acc[6] = bf16_lo(x.w); acc[7] = bf16_hi(x.w);
+}
+
+__device__ __forceinline__ void store_avg8(float* d, const float (&acc)[8], float wf) {
+    stf16(d, make_float4(acc[0] / wf, acc[1] / wf, acc[2] / wf, acc[3] / wf));
+    stf16(d + 4, make_float4(acc[4] / wf, acc[5] / wf, acc[6] / wf, acc[7] / wf));
+}
+
+// Loads of sources i0 .. i0+kReduceBatch-1 (those below W unless kFull) of a
+// full tile; all are issued before any of them is used.
+template <bool kFull>
+__device__ __forceinline__ void load_sources(uint4 (&x)[kReduceBatch][kReduceSteps], const uint16_t* tile,
+                                             int i0, int W, int64_t S, uint32_t t) {
+    constexpr uint32_t kStride = uint32_t(kReduceBlock) * kVec;
+#pragma unroll
+    for (int b = 0; b < kReduceBatch; ++b) {
+        if (kFull || i0 + b < W) {
+            const uint16_t* src = tile + int64_t(i0 + b) * S;
+#pragma unroll
+            for (int u = 0; u < kReduceSteps; ++u) x[b][u] = ld16(src + t + u * kStride);
+        }
+    }
+}
+
+// A full tile: kReduceSteps groups of 8 outputs per thread, spaced kReduceBlock*kVec
+// apart.  `tile` is the wave-uniform start of the tile in rank 0's chunk.  The
+// W sources of every output are added in rank order 0..W-1, starting from
+// source 0; the loads of kReduceBatch sources are issued ahead of their adds.
+__device__ __forceinline__ void reduce_tile_vec(const uint16_t* __restrict__ tile, float* __restrict__ dtile,
+                                                int W, int64_t S, float wf) {
+    constexpr uint32_t kStride = uint32_t(kReduceBlock) * kVec;
+    const uint32_t t = threadIdx.x * kVec;
+    float acc[kReduceSteps][8];
+    uint4 x[kReduceBatch][kReduceSteps];
+    if (W >= kReduceBatch) load_sources<true>(x, tile, 0, W, S, t);
+    else load_sources<false>(x, tile, 0, W, S, t);
+#pragma unroll
+    for (int u = 0; u < kReduceSteps; ++u) init8(acc[u], x[0][u]);
+#pragma unroll
+    for (int b = 1; b < kReduceBatch; ++b)
+        if (b < W) {
+#pragma unroll
+            for (int u = 0; u < kReduceSteps; ++u) add8(acc[u], x[b][u]);
+        }
+    int i = kReduceBatch;
+    for (; i + kReduceBatch <= W; i += kReduceBatch) {
+        load_sources<true>(x, tile, i, W, S, t);
+#pragma unroll
+        for (int b = 0; b < kReduceBatch; ++b)
+#pragma unroll
+            for (int u = 0; u < kReduceSteps; ++u) add8(acc[u], x[b][u]);
+    }
+    if (i < W) {
+        load_sources<false>(x, tile, i, W, S, t);
+#pragma unroll
+        for (int b = 0; b < kReduceBatch; ++b)
+            if (i + b < W) {
+#pragma unroll
+                for (int u = 0; u < kReduceSteps; ++u) add8(acc[u], x[b][u]);
+            }
+    }
+#pragma unroll
+    for (int u = 0; u < kReduceSteps; ++u) store_avg8(dtile + t + u * kStride, acc[u], wf);
+}
+
+__global__ void __launch_bounds__(kReduceBlock) rs_reduce_kernel(const ReduceArgs a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     const int W = a.world;
@@ -275,36 +394,32 @@ __global__ void __launch_bounds__(kBlock) rs_reduce_kernel(const ReduceArgs a) {
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
         const int p = param_of_tile(my_start, t);
         const int64_t v = a.valid[p];
-        const int64_t g = int64_t(t - a.tile_start[p]) * kReduceTile + int64_t(threadIdx.x) * kVec;
-        if (g >= v) continue;
-        const uint16_t* __restrict__ s = a.src + a.off[p] + g;
-        float* __restrict__ d = a.dst[p] + g;
+        const int64_t lo = int64_t(t - a.tile_start[p]) * kReduceTile;
+        const uint16_t* __restrict__ s0 = a.src + a.off[p];
+        float* __restrict__ d0 = a.dst[p];
         const bool vec = ((a.dst_aligned >> p) & 1) && ((a.off[p] | S) & (kVec - 1)) == 0;
-        if (vec && g + kVec <= v) {
-            const uint4 x0 = ld16(s);
-            float acc[8] = {bf16_lo(x0.x), bf16_hi(x0.x), bf16_lo(x0.y), bf16_hi(x0.y),
-                            bf16_lo(x0.z), bf16_hi(x0.z), bf16_lo(x0.w), bf16_hi(x0.w)};
-            int i = 1;
-            for (; i + kReduceBatch <= W; i += kReduceBatch) {
-                uint4 x[kReduceBatch];
-#pragma unroll
-                for (int b = 0; b < kReduceBatch; ++b) x[b] = ld16(s + int64_t(i + b) * S);
-#pragma unroll
-                for (int b = 0; b < kReduceBatch; ++b) add8(acc, x[b]);
-            }
-            for (; i < W; ++i) add8(acc, ld16(s + int64_t(i) * S));
-            float4 o0, o1;
-            o0.x = acc[0] / wf; o0.y = acc[1] / wf; o0.z = acc[2] / wf; o0.w = acc[3] / wf;
-            o1.x = acc[4] / wf; o1.y = acc[5] / wf; o1.z = acc[6] / wf; o1.w = acc[7] / wf;
-            *reinterpret_cast<float4*>(d) = o0;
-            *reinterpret_cast<float4*>(d + 4) = o1;
+        if (vec && lo + kReduceTile <= v) {
+            reduce_tile_vec(s0 + lo, d0 + lo, W, S, wf);
             continue;
         }
-        for (int e = 0; e < kVec; ++e) {
-            if (g + e >= v) break;
-            float acc = bf16_lo(s[e]);
-            for (int i = 1; i < W; ++i) acc += bf16_lo(s[int64_t(i) * S + e]);
-            d[e] = acc / wf;
+        for (int u = 0; u < kReduceSteps; ++u) {
+            const int64_t g = lo + (int64_t(u) * kReduceBlock + threadIdx.x) * kVec;
+            if (g >= v) break;
+            const uint16_t* __restrict__ s = s0 + g;
+            float* __restrict__ d = d0 + g;
+            if (vec && g + kVec <= v) {
+                float acc[8];
+                init8(acc, ld16(s));
+                for (int i = 1; i < W; ++i) add8(acc, ld16(s + int64_t(i) * S));
+                store_avg8(d, acc, wf);
+                continue;
+            }
+            for (int e = 0; e < kVec; ++e) {
+                if (g + e >= v) break;
+                float acc = bf16_lo(s[e]);
+                for (int i = 1; i < W; ++i) acc += bf16_lo(s[int64_t(i) * S + e]);
+                d[e] = acc / wf;
+            }
         }
     }
 }
@@ -376,14 +491,14 @@ const Plan* get_plan(const fsdp_plan* h, fsdp_status* st) {
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 template <typename Args>
-fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, hipStream_t stream) {
+fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream) {
     if (ntiles == 0) return FSDP_OK;
     fsdp_status st = FSDP_OK;
     const int cus = cu_count(&st);
     if (st != FSDP_OK) return st;
     const int grid = std::min(ntiles, cus * kBlocksPerCU);
     void* kargs[] = {const_cast<Args*>(&args)};
-    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), dim3(grid), dim3(kBlock),
+    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), dim3(grid), dim3(block),
                                          kargs, 0, stream);
     if (e != hipSuccess) return fail(FSDP_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
     return FSDP_OK;
@@ -426,7 +541,7 @@ extern "C" fsdp_status fsdp_ag_pack(const fsdp_plan* h, int32_t rank, const floa
     if (pl->chunk > 0 &&
         (st = check_overlap({{uintptr_t(send_chunk), uintptr_t(send_chunk + pl->chunk), -1}}, ins)) != FSDP_OK)
         return st;
-    return launch(ag_pack_kernel, a, nt, stream);
+    return launch(ag_pack_kernel, a, nt, kCopyBlock, stream);
 }
 
 extern "C" fsdp_status fsdp_ag_unpack(const fsdp_plan* h, const uint16_t* gathered, uint16_t* const* params,
@@ -461,7 +576,7 @@ extern "C" fsdp_status fsdp_ag_unpack(const fsdp_plan* h, const uint16_t* gather
     std::vector<Span> ins;
     if (total > 0) ins.push_back({uintptr_t(gathered), uintptr_t(gathered + total), -1});
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    return launch(ag_unpack_kernel, a, nt, stream);
+    return launch(ag_unpack_kernel, a, nt, kCopyBlock, stream);
 }
 
 extern "C" fsdp_status fsdp_rs_pack(const fsdp_plan* h, const uint16_t* const* grads, uint16_t* send_buf,
@@ -497,7 +612,7 @@ extern "C" fsdp_status fsdp_rs_pack(const fsdp_plan* h, const uint16_t* const* g
     if (total > 0 &&
         (st = check_overlap({{uintptr_t(send_buf), uintptr_t(send_buf + total), -1}}, ins)) != FSDP_OK)
         return st;
-    return launch(rs_pack_kernel, a, nt, stream);
+    return launch(rs_pack_kernel, a, nt, kCopyBlock, stream);
 }
 
 extern "C" fsdp_status fsdp_rs_reduce(const fsdp_plan* h, int32_t rank, const uint16_t* recv,
@@ -532,5 +647,5 @@ extern "C" fsdp_status fsdp_rs_reduce(const fsdp_plan* h, int32_t rank, const ui
     std::vector<Span> ins;
     if (total > 0) ins.push_back({uintptr_t(recv), uintptr_t(recv + total), -1});
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    return launch(rs_reduce_kernel, a, nt, stream);
+    return launch(rs_reduce_kernel, a, nt, kReduceBlock, stream);
 }

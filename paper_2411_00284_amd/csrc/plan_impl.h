@@ -9,13 +9,30 @@
 
 namespace fsdp {
 
-// Output elements handled by one work tile of the copy kernels and of the
-// reduction (a 256-thread workgroup, 8 elements = 16 bytes per thread and
-// step; the copy kernels take 4 steps per tile, the reduction 1).
-constexpr int kBlock = 256;
+// Work tiles.  The copy kernels (ag_pack, ag_unpack, rs_pack) run
+// kCopyBlock threads that move 8 elements (16 bytes of bf16) per thread and
+// step, kCopySteps steps per tile; the reduction runs kReduceBlock threads
+// that each own kReduceSteps groups of 8 outputs.  One tile per workgroup
+// (small tiles, many workgroups) measured fastest for these HBM streams.
+#ifndef FSDP_COPY_BLOCK
+#define FSDP_COPY_BLOCK 128
+#endif
+#ifndef FSDP_COPY_STEPS
+#define FSDP_COPY_STEPS 2
+#endif
+#ifndef FSDP_REDUCE_BLOCK
+#define FSDP_REDUCE_BLOCK 256
+#endif
+#ifndef FSDP_REDUCE_STEPS
+#define FSDP_REDUCE_STEPS 2
+#endif
 constexpr int kVec = 8;
-constexpr int64_t kCopyTile = int64_t(kBlock) * kVec * 4;
-constexpr int64_t kReduceTile = int64_t(kBlock) * kVec;
+constexpr int kCopyBlock = FSDP_COPY_BLOCK;
+constexpr int kCopySteps = FSDP_COPY_STEPS;
+constexpr int64_t kCopyTile = int64_t(kCopyBlock) * kVec * kCopySteps;
+constexpr int kReduceBlock = FSDP_REDUCE_BLOCK;
+constexpr int kReduceSteps = FSDP_REDUCE_STEPS;
+constexpr int64_t kReduceTile = int64_t(kReduceBlock) * kVec * kReduceSteps;
 
 struct Plan {
     int32_t world;     // W
