@@ -224,20 +224,16 @@ def main(argv=None):
     return 0
 
 
-def cpu_baseline(wl):
-    """The oracle, as it stands, on a bounded sample of the workload: the same
-    world size and parameter shapes, restricted to the attention projections
-    and norms (wq, wk, wv, wo and both norms) when the block has them."""
+def cpu_baseline(wl, min_seconds=10.0, max_passes=50):
+    """The oracle, as it stands, timed on the host: all four steps at rank 0
+    over the whole bucket, repeated until about ``min_seconds`` of CPU work
+    has been measured (the oracle is single-threaded numpy)."""
     import numpy as np
 
     import oracle.fsdp_oracle as O
     from synth import random_bits16, random_bits32
 
-    names = set(wl.names)
-    keep = [p for p, nm in enumerate(wl.names) if nm in ("wq", "wk", "wv", "wo", "attention_norm", "ffn_norm")]
-    if len(keep) < 2 or not {"wq", "wo"} <= names:
-        keep = list(range(wl.num_params))
-    dims = [wl.dims[p] for p in keep]
+    dims = list(wl.dims)
     W = wl.world_size
     plan = O.make_plan(W, dims, 8)
     S = plan.chunk
@@ -248,23 +244,26 @@ def cpu_baseline(wl):
     gathered = random_bits16([2], W * S)
     grads = [random_bits16([3, p], n * k).reshape(n, k) for p, (n, k) in enumerate(dims)]
     recv = (random_bits16([4], W * S) & np.uint16(0xBFFF))      # finite: exponent MSB cleared
-    t = {}
-    t0 = time.perf_counter(); O.ag_pack(plan, 0, shards); t["ag_pack"] = time.perf_counter() - t0
-    t0 = time.perf_counter(); O.ag_unpack(plan, gathered); t["ag_unpack"] = time.perf_counter() - t0
-    t0 = time.perf_counter(); O.rs_pack(plan, grads); t["rs_pack"] = time.perf_counter() - t0
-    t0 = time.perf_counter(); O.rs_reduce(plan, 0, recv); t["rs_reduce"] = time.perf_counter() - t0
+    t = {k: 0.0 for k in ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")}
+    passes = 0
+    while passes < max_passes and (passes == 0 or sum(t.values()) < min_seconds):
+        t0 = time.perf_counter(); O.ag_pack(plan, 0, shards); t["ag_pack"] += time.perf_counter() - t0
+        t0 = time.perf_counter(); O.ag_unpack(plan, gathered); t["ag_unpack"] += time.perf_counter() - t0
+        t0 = time.perf_counter(); O.rs_pack(plan, grads); t["rs_pack"] += time.perf_counter() - t0
+        t0 = time.perf_counter(); O.rs_reduce(plan, 0, recv); t["rs_reduce"] += time.perf_counter() - t0
+        passes += 1
     b = algorithmic_bytes(W, S, E, V0)
     total_s = sum(t.values())
     return {
-        "value": round(sum(b.values()) / total_s / 1e9, 3),
+        "value": round(passes * sum(b.values()) / total_s / 1e9, 3),
         "unit": "GB/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": (f"{wl.name}: params {[wl.names[p] for p in keep]} (W={W}, {E} elements, "
-                   f"{sum(b.values())} algorithmic bytes), all four steps at rank 0, numpy single thread; "
+        "sample": (f"{wl.name}: the whole bucket ({len(dims)} params, W={W}, {sum(b.values())} algorithmic "
+                   f"bytes per pass), all four steps at rank 0, {passes} passes, numpy single thread; "
                    f"host has {len(os.sched_getaffinity(0))} cores"),
         "seconds": round(total_s, 3),
-        "per_kernel_s": {k: round(v, 3) for k, v in t.items()},
+        "per_pass_s": {k: round(v / passes, 4) for k, v in t.items()},
     }
 
 
