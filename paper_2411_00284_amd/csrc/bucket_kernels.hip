@@ -50,6 +50,7 @@ namespace {
 constexpr int PMAX = FSDP_MAX_PARAMS;
 constexpr int kReduceBatch = FSDP_REDUCE_BATCH;   // source ranks loaded before they are added
 constexpr int kBlocksPerCU = FSDP_BLOCKS_PER_CU;  // workgroups per CU in the grid-stride launch
+constexpr int kPackGridSlack = 4;                  // max workgroups per tile of work for the 2-D pack grid
 
 // ------------------------------------------------------------------ device helpers
 
@@ -134,42 +135,59 @@ __device__ __forceinline__ uint4 cast8(const float* __restrict__ s) {
                       bf16x2_bits(b.x, b.y), bf16x2_bits(b.z, b.w));
 }
 
+// Tile lt of parameter p: cast-and-pack its part of [off_p, off_{p+1}).
+__device__ __forceinline__ void pack_tile(const PackArgs& a, int p, int lt) {
+    const int64_t off = a.off[p];
+    const int64_t region = a.off[p + 1] - off;
+    const int64_t valid = a.valid[p];
+    const float* __restrict__ src = a.src[p];
+    uint16_t* __restrict__ dst = a.dst + off;
+    const int64_t lo = int64_t(lt) * kPackTile;
+    const int64_t hi = min(lo + kPackTile, region);
+    if (lo >= hi) return;
+    const bool vec = (a.vec_mask >> p) & 1;
+    if (vec && hi - lo == kPackTile && lo + kPackTile <= valid) {
+        uint4 v[kPackSteps];
+#pragma unroll
+        for (int u = 0; u < kPackSteps; ++u)
+            v[u] = cast8(src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec);
+#pragma unroll
+        for (int u = 0; u < kPackSteps; ++u)
+            st16(dst + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec, v[u]);
+        return;
+    }
+    for (int u = 0; u < kPackSteps; ++u) {
+        const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
+        if (g >= hi) break;
+        if (vec && g + kVec <= hi && (g + kVec <= valid || g >= valid)) {
+            st16(dst + g, g < valid ? cast8(src + g) : make_uint4(0, 0, 0, 0));
+            continue;
+        }
+        for (int e = 0; e < kVec; ++e) {
+            const int64_t k = g + e;
+            if (k < hi) dst[k] = k < valid ? uint16_t(bf16_bits(src[k])) : uint16_t(0);
+        }
+    }
+}
+
+// Tiles numbered across the bucket; the parameter of a tile comes from the
+// wave-ballot lookup.
 __global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
         const int p = param_of_tile(my_start, t);
-        const int64_t off = a.off[p];
-        const int64_t region = a.off[p + 1] - off;
-        const int64_t valid = a.valid[p];
-        const float* __restrict__ src = a.src[p];
-        uint16_t* __restrict__ dst = a.dst + off;
-        const int64_t lo = int64_t(t - a.tile_start[p]) * kCopyTile;
-        const int64_t hi = min(lo + kCopyTile, region);
-        const bool vec = (a.vec_mask >> p) & 1;
-        if (vec && hi - lo == kCopyTile && lo + kCopyTile <= valid) {
-            uint4 v[kCopySteps];
-#pragma unroll
-            for (int u = 0; u < kCopySteps; ++u)
-                v[u] = cast8(src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec);
-#pragma unroll
-            for (int u = 0; u < kCopySteps; ++u)
-                st16(dst + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec, v[u]);
-            continue;
-        }
-        for (int u = 0; u < kCopySteps; ++u) {
-            const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
-            if (g >= hi) break;
-            if (vec && g + kVec <= hi && (g + kVec <= valid || g >= valid)) {
-                st16(dst + g, g < valid ? cast8(src + g) : make_uint4(0, 0, 0, 0));
-                continue;
-            }
-            for (int e = 0; e < kVec; ++e) {
-                const int64_t k = g + e;
-                if (k < hi) dst[k] = k < valid ? uint16_t(bf16_bits(src[k])) : uint16_t(0);
-            }
-        }
+        pack_tile(a, p, t - a.tile_start[p]);
     }
+}
+
+// Grid (x, P): blockIdx.y is the parameter, so a workgroup's first memory
+// access is its data rather than the tile table.  Used when the parameters'
+// tile counts are similar enough that few workgroups find no tile.
+__global__ void __launch_bounds__(kCopyBlock) ag_pack_grid_kernel(const PackArgs a) {
+    const int p = blockIdx.y;
+    const int nt = int((a.off[p + 1] - a.off[p] + kPackTile - 1) / kPackTile);
+    for (int lt = blockIdx.x; lt < nt; lt += gridDim.x) pack_tile(a, p, lt);
 }
 
 // ------------------------------------------------------------------ ag_unpack
@@ -490,15 +508,21 @@ const Plan* get_plan(const fsdp_plan* h, fsdp_status* st) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
+// One launch of `kernel` over `ntiles` work tiles (grid-stride beyond
+// kBlocksPerCU workgroups per CU).  A 2-D launch passes grid.y and the tile
+// count of its x dimension.
 template <typename Args>
-fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream) {
+fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream,
+                   dim3 grid2 = dim3(0, 1), int xtiles = 0) {
     if (ntiles == 0) return FSDP_OK;
     fsdp_status st = FSDP_OK;
     const int cus = cu_count(&st);
     if (st != FSDP_OK) return st;
-    const int grid = std::min(ntiles, cus * kBlocksPerCU);
+    const dim3 grid = grid2.y > 1 || xtiles > 0
+                          ? dim3(std::min(xtiles, cus * kBlocksPerCU), grid2.y)
+                          : dim3(std::min(ntiles, cus * kBlocksPerCU));
     void* kargs[] = {const_cast<Args*>(&args)};
-    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), dim3(grid), dim3(block),
+    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(block),
                                          kargs, 0, stream);
     if (e != hipSuccess) return fail(FSDP_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
     return FSDP_OK;
@@ -522,7 +546,7 @@ extern "C" fsdp_status fsdp_ag_pack(const fsdp_plan* h, int32_t rank, const floa
     if ((st = check_bucket_ptr(send_chunk, pl->chunk, "send_chunk")) != FSDP_OK) return st;
     PackArgs a{};
     std::vector<Span> ins;
-    int32_t nt = 0;
+    int32_t nt = 0, max_tiles = 0;
     for (int p = 0; p < pl->nparams; ++p) {
         const int64_t v = pl->local_elems(p, rank);
         if ((st = check_param_ptr(shards[p], v, 4, p, "shards")) != FSDP_OK) return st;
@@ -530,7 +554,8 @@ extern "C" fsdp_status fsdp_ag_pack(const fsdp_plan* h, int32_t rank, const floa
         a.off[p] = pl->off[p];
         a.valid[p] = v;
         a.tile_start[p] = nt;
-        nt += tiles(pl->off[p + 1] - pl->off[p], kCopyTile);
+        nt += tiles(pl->off[p + 1] - pl->off[p], kPackTile);
+        max_tiles = std::max(max_tiles, tiles(pl->off[p + 1] - pl->off[p], kPackTile));
         if (aligned16(shards[p]) && (pl->off[p] & (kVec - 1)) == 0) a.vec_mask |= uint64_t(1) << p;
         if (v > 0) ins.push_back({uintptr_t(shards[p]), uintptr_t(shards[p] + v), p});
     }
@@ -541,6 +566,9 @@ extern "C" fsdp_status fsdp_ag_pack(const fsdp_plan* h, int32_t rank, const floa
     if (pl->chunk > 0 &&
         (st = check_overlap({{uintptr_t(send_chunk), uintptr_t(send_chunk + pl->chunk), -1}}, ins)) != FSDP_OK)
         return st;
+    // the 2-D grid launches P * max_tiles workgroups for nt tiles of work
+    if (int64_t(pl->nparams) * max_tiles <= kPackGridSlack * int64_t(nt))
+        return launch(ag_pack_grid_kernel, a, nt, kCopyBlock, stream, dim3(0, pl->nparams), max_tiles);
     return launch(ag_pack_kernel, a, nt, kCopyBlock, stream);
 }
 

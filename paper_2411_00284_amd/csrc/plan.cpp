@@ -103,7 +103,7 @@ extern "C" fsdp_status fsdp_bucket_plan(int32_t world_size, int32_t num_params,
     int64_t t_pack = 0, t_copy = 0, t_reduce = 0;
     for (int p = 0; p < num_params; ++p) {
         const int64_t region = pl.off[p + 1] - pl.off[p];
-        t_pack += (region + kCopyTile - 1) / kCopyTile;
+        t_pack += (region + kPackTile - 1) / kPackTile;
         t_copy += W * ((region + kCopyTile - 1) / kCopyTile);
         t_reduce += (pl.seg[p] + kReduceTile - 1) / kReduceTile;
     }

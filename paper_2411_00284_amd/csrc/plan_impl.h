@@ -11,14 +11,17 @@ namespace fsdp {
 
 // Work tiles.  The copy kernels (ag_pack, ag_unpack, rs_pack) run
 // kCopyBlock threads that move 8 elements (16 bytes of bf16) per thread and
-// step, kCopySteps steps per tile; the reduction runs kReduceBlock threads
-// that each own kReduceSteps groups of 8 outputs.  One tile per workgroup
+// step, kCopySteps steps per tile (kPackSteps for ag_pack); the reduction
+// runs kReduceBlock threads that each own kReduceSteps groups of 8 outputs.  One tile per workgroup
 // (small tiles, many workgroups) measured fastest for these HBM streams.
 #ifndef FSDP_COPY_BLOCK
 #define FSDP_COPY_BLOCK 128
 #endif
 #ifndef FSDP_COPY_STEPS
 #define FSDP_COPY_STEPS 2
+#endif
+#ifndef FSDP_PACK_STEPS
+#define FSDP_PACK_STEPS 1
 #endif
 #ifndef FSDP_REDUCE_BLOCK
 #define FSDP_REDUCE_BLOCK 256
@@ -30,6 +33,8 @@ constexpr int kVec = 8;
 constexpr int kCopyBlock = FSDP_COPY_BLOCK;
 constexpr int kCopySteps = FSDP_COPY_STEPS;
 constexpr int64_t kCopyTile = int64_t(kCopyBlock) * kVec * kCopySteps;
+constexpr int kPackSteps = FSDP_PACK_STEPS;
+constexpr int64_t kPackTile = int64_t(kCopyBlock) * kVec * kPackSteps;
 constexpr int kReduceBlock = FSDP_REDUCE_BLOCK;
 constexpr int kReduceSteps = FSDP_REDUCE_STEPS;
 constexpr int64_t kReduceTile = int64_t(kReduceBlock) * kVec * kReduceSteps;

@@ -41,6 +41,8 @@ SMALL = [
     (5, [(40000, 3), (9, 4096)]),
     # the parameter limit
     (4, [(i % 13, 1 + i % 5) for i in range(64)]),
+    # one large and many tiny parameters (the pack kernel's tile-lookup grid)
+    (2, [(200000, 1)] + [(1, 1)] * 8),
 ]
 
 
