@@ -185,30 +185,40 @@ def bf16_to_f32(bits) -> np.ndarray:
 # Forward: all-gather copy-in / exchange / copy-out
 # --------------------------------------------------------------------------
 
-def ag_pack(plan: Plan, rank: int, shards: Sequence[np.ndarray]) -> np.ndarray:
+def ag_pack(plan: Plan, rank: int, shards: Sequence[np.ndarray], param_dtype: str = "bf16") -> np.ndarray:
     """O1, all-gather copy-in of one rank (section 3.2.1; section 4 param_dtype).
 
     ``shards[p]`` is the rank's unpadded fp32 Shard(0) slab of parameter p,
-    n_{p,rank} x inner_p.  Output: the rank's bf16 chunk of S elements, with
-    shard p cast to bf16 at off_p and zeros everywhere else (pad rows, gaps,
-    tail).
+    n_{p,rank} x inner_p.  Output: the rank's chunk of S elements, with shard p
+    cast to ``param_dtype`` at off_p and zeros everywhere else (pad rows, gaps,
+    tail).  ``param_dtype`` is "bf16" (mixed precision: bf16 bit patterns as
+    uint16) or "f32" (no mixed precision: the fp32 values themselves).
     """
     if not 0 <= rank < plan.world_size:
         raise ValueError("rank out of range")
-    send = np.zeros(plan.chunk, dtype=np.uint16)
+    out_dtype = _wire_dtype(param_dtype)
+    send = np.zeros(plan.chunk, dtype=out_dtype)
     for p in range(plan.num_params):
         v = local_elems(plan, p, rank)
         src = np.asarray(shards[p], dtype=np.float32).reshape(-1)
         if src.size != v:
             raise ValueError(f"shard {p} has {src.size} elements, expected {v}")
         o = plan.offset[p]
-        send[o:o + v] = bf16_rne(src)
+        send[o:o + v] = bf16_rne(src) if param_dtype == "bf16" else src
     return send
+
+
+def _wire_dtype(name: str):
+    if name == "bf16":
+        return np.uint16
+    if name == "f32":
+        return np.float32
+    raise ValueError("dtype must be 'bf16' or 'f32'")
 
 
 def all_gather(chunks: Sequence[np.ndarray]) -> np.ndarray:
     """O2, the exchange (not on the GPU path): gathered[i*S + k] = chunk_i[k]."""
-    return np.concatenate([np.asarray(c, dtype=np.uint16).reshape(-1) for c in chunks])
+    return np.concatenate([np.asarray(c).reshape(-1) for c in chunks])
 
 
 def ag_unpack(plan: Plan, gathered: np.ndarray) -> list[np.ndarray]:
@@ -218,16 +228,17 @@ def ag_unpack(plan: Plan, gathered: np.ndarray) -> list[np.ndarray]:
     row q = row % c_p of p's segment: element (row, col) is
     gathered[i*S + off_p + q*inner_p + col].  Rows of one rank are contiguous
     on both sides, so each rank's rows move as one slice.  Output: the full,
-    unpadded bf16 parameters, rows x inner.
+    unpadded parameters, rows x inner, in the gathered buffer's element type
+    (bf16 bit patterns or fp32).
     """
     W, S = plan.world_size, plan.chunk
-    g = np.asarray(gathered, dtype=np.uint16).reshape(-1)
+    g = np.asarray(gathered).reshape(-1)
     if g.size != W * S:
         raise ValueError("gathered buffer must hold W*S elements")
     out = []
     for p in range(plan.num_params):
         n, k, c, o = plan.rows[p], plan.inner[p], plan.rows_per_rank[p], plan.offset[p]
-        full = np.empty((n, k), dtype=np.uint16)
+        full = np.empty((n, k), dtype=g.dtype)
         for i in range(W):
             ni = local_rows(plan, p, i)
             if ni == 0:
@@ -242,21 +253,31 @@ def ag_unpack(plan: Plan, gathered: np.ndarray) -> list[np.ndarray]:
 # Backward: reduce-scatter copy-in / exchange / reduction with read-out
 # --------------------------------------------------------------------------
 
-def rs_pack(plan: Plan, grads: Sequence[np.ndarray]) -> np.ndarray:
-    """O4, reduce-scatter copy-in (section 3.2.1).
+def rs_pack(plan: Plan, grads: Sequence[np.ndarray], reduce_dtype: str | None = None) -> np.ndarray:
+    """O4, reduce-scatter copy-in (section 3.2.1; section 4 reduce_dtype).
 
-    Each full bf16 gradient G_p (rows x inner) is zero-padded along dim 0 to
+    Each full gradient G_p (rows x inner) is zero-padded along dim 0 to
     W * c_p rows and split into W chunks of c_p rows; chunk j goes to
     destination j's part of the send buffer at j*S + off_p.  Everything the
-    chunks do not cover is zero.
+    chunks do not cover is zero.  Gradients are bf16 bit patterns (uint16) or
+    fp32.  ``reduce_dtype="f32"`` casts bf16 gradients to fp32 first (an exact
+    widening); by default the buffer keeps the gradients' own type.
     """
     W, S = plan.world_size, plan.chunk
-    send = np.zeros(W * S, dtype=np.uint16)
+    gs = [np.asarray(g) for g in grads]
+    if reduce_dtype == "f32":
+        gs = [bf16_to_f32(g) if g.dtype == np.uint16 else g.astype(np.float32) for g in gs]
+    elif reduce_dtype not in (None, "bf16"):
+        raise ValueError("reduce_dtype must be 'bf16' or 'f32'")
+    dtype = gs[0].dtype if gs else np.uint16
+    if reduce_dtype == "bf16" and dtype != np.uint16:
+        raise ValueError("a bf16 wire needs bf16 gradients")
+    send = np.zeros(W * S, dtype=dtype)
     for p in range(plan.num_params):
         n, k, c, L, o = (plan.rows[p], plan.inner[p], plan.rows_per_rank[p],
                          plan.seg[p], plan.offset[p])
-        G = np.asarray(grads[p], dtype=np.uint16).reshape(n, k)
-        padded = np.zeros((W * c, k), dtype=np.uint16)
+        G = gs[p].astype(dtype, copy=False).reshape(n, k)
+        padded = np.zeros((W * c, k), dtype=dtype)
         padded[:n] = G
         flat = padded.reshape(-1)
         for j in range(W):
@@ -266,22 +287,24 @@ def rs_pack(plan: Plan, grads: Sequence[np.ndarray]) -> np.ndarray:
 
 def rs_exchange(send_bufs: Sequence[np.ndarray], rank: int, chunk: int) -> np.ndarray:
     """O5, the exchange (not on the GPU path): recv[i*S + k] = send_i[rank*S + k]."""
-    return np.concatenate([np.asarray(b, dtype=np.uint16).reshape(-1)[rank * chunk:(rank + 1) * chunk]
+    return np.concatenate([np.asarray(b).reshape(-1)[rank * chunk:(rank + 1) * chunk]
                            for b in send_bufs])
 
 
 def rs_reduce(plan: Plan, rank: int, recv: np.ndarray) -> list[np.ndarray]:
     """O6, the rank-local average and read-out (section 3.2.1; section 4 reduce_dtype).
 
-    For every element of the rank's Shard(0) slab of parameter p: widen the
-    W incoming bf16 values x_0..x_{W-1} to fp32 (exact), start from x_0, add
-    x_1, ..., x_{W-1} one at a time in fp32, then divide once by W in fp32.
-    Output: the fp32 gradient shards, n_{p,rank} x inner_p (no padded rows).
+    For every element of the rank's Shard(0) slab of parameter p: take the W
+    incoming values x_0..x_{W-1} in fp32 (bf16 bit patterns are widened,
+    exactly; an fp32 buffer is used as it is), start from x_0, add x_1, ...,
+    x_{W-1} one at a time in fp32, then divide once by W in fp32.  Output: the
+    fp32 gradient shards, n_{p,rank} x inner_p (no padded rows).
     """
     W, S = plan.world_size, plan.chunk
     if not 0 <= rank < W:
         raise ValueError("rank out of range")
-    r = np.asarray(recv, dtype=np.uint16).reshape(-1)
+    r = np.asarray(recv).reshape(-1)
+    widen = bf16_to_f32 if r.dtype == np.uint16 else (lambda a: np.asarray(a, dtype=np.float32))
     if r.size != W * S:
         raise ValueError("recv buffer must hold W*S elements")
     wf = np.float32(W)
@@ -289,9 +312,9 @@ def rs_reduce(plan: Plan, rank: int, recv: np.ndarray) -> list[np.ndarray]:
     for p in range(plan.num_params):
         n, k, o = local_rows(plan, p, rank), plan.inner[p], plan.offset[p]
         v = n * k
-        acc = bf16_to_f32(r[o:o + v])
+        acc = widen(r[o:o + v]).copy()
         for i in range(1, W):
-            x = bf16_to_f32(r[i * S + o:i * S + o + v])
+            x = widen(r[i * S + o:i * S + o + v])
             acc = np.add(acc, x, dtype=np.float32)
         res = np.divide(acc, wf, dtype=np.float32)
         out.append(res.reshape(n, k))

@@ -424,3 +424,75 @@ def check_rs_exact_mean_bound(impl, w, seed):
     mean = x.sum(axis=0) / w
     bound = (w - 1) * 2.0 ** -24 * np.abs(x).sum(axis=0) / w + np.abs(mean) * 2.0 ** -24 + 1e-45
     assert np.all(np.abs(out - mean) <= bound)
+
+
+# ---------------------------------------------------------------- fp32 variants
+
+def check_f32_param_roundtrip(impl, w, dims, seed, align=8):
+    """Without mixed precision (param_dtype fp32) the all-gather reproduces the
+    fp32 parameter bit for bit, NaN payloads included."""
+    plan = impl.make_plan(w, dims, align)
+    xs = [f32_from_bits(random_bits32([seed, p, 11], n * k)).reshape(n, k) for p, (n, k) in enumerate(dims)]
+    chunks = []
+    for r in range(w):
+        local = []
+        for p, (n, k) in enumerate(dims):
+            parts = torch.chunk(torch.from_numpy(xs[p]), w, dim=0) if n else ()
+            local.append(parts[r].numpy() if r < len(parts) else np.zeros((0, k), np.float32))
+        send = impl.ag_pack(plan, r, local, param_dtype="f32")
+        assert send.dtype == np.float32 and send.shape == (plan.chunk,)
+        # padding is +0.0 in fp32 too
+        mask = np.ones(plan.chunk, bool)
+        for p in range(len(dims)):
+            v = impl.local_rows(plan, p, r) * dims[p][1]
+            mask[plan.offset[p]:plan.offset[p] + v] = False
+        assert np.all(send.view(np.uint32)[mask] == 0)
+        chunks.append(send)
+    out = impl.ag_unpack(plan, np.concatenate(chunks))
+    for p in range(len(dims)):
+        assert out[p].dtype == np.float32
+        assert np.array_equal(out[p].view(np.uint32), xs[p].view(np.uint32)), p
+
+
+def check_f32_wire_same_bits(impl, w, dims, seed, align=8):
+    """An fp32 reduce-scatter wire (gradients cast to reduce_dtype before the
+    exchange) gives the same result bits as the bf16 wire: widening is exact."""
+    plan = impl.make_plan(w, dims, align)
+    S = plan.chunk
+    rng = np.random.default_rng([seed, 12])
+    grads = []
+    for i in range(w):
+        gi = []
+        for n, k in dims:
+            f = rng.standard_normal((n, k)) * np.exp2(rng.integers(-24, 25, (n, k)))
+            gi.append((f.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16))
+        grads.append(gi)
+    s16 = [impl.rs_pack(plan, g) for g in grads]
+    s32 = [impl.rs_pack(plan, g, reduce_dtype="f32") for g in grads]
+    for a, b in zip(s16, s32):
+        assert b.dtype == np.float32
+        assert np.array_equal((a.astype(np.uint32) << 16), b.view(np.uint32))
+    for j in sorted({0, w // 2, w - 1}):
+        r16 = impl.rs_reduce(plan, j, _exchange(s16, j, S))
+        r32 = impl.rs_reduce(plan, j, _exchange(s32, j, S))
+        for p in range(len(dims)):
+            assert np.array_equal(r16[p].view(np.uint32), r32[p].view(np.uint32)), (j, p)
+
+
+def check_rs_reduce_bruteforce_f32(impl, w, dims, rank, seed, align=8):
+    """fp32 inputs (full 24-bit significands, wide exponents): the same
+    binary64-rounded-per-step brute force as for bf16 inputs."""
+    plan = impl.make_plan(w, dims, align)
+    S = plan.chunk
+    rng = np.random.default_rng([seed, 13])
+    recv = (rng.standard_normal(w * S) * np.exp2(rng.integers(-30, 31, w * S))).astype(np.float32)
+    out = impl.rs_reduce(plan, rank, recv)
+    for p, (n, k) in enumerate(dims):
+        nr = impl.local_rows(plan, p, rank)
+        flat = out[p].reshape(-1)
+        assert flat.size == nr * k
+        for e in range(nr * k):
+            a = float(recv[plan.offset[p] + e])
+            for i in range(1, w):
+                a = round_f32(a + float(recv[i * S + plan.offset[p] + e]))
+            assert float(flat[e]) == round_f32(a / w), (p, e)

@@ -11,6 +11,10 @@ path (pack, exchange, unpack; pack, exchange, reduce) must reproduce it:
 * reduce-scatter average: bit-exact whenever the fp32 sum is order-free,
   i.e. for W = 2 with arbitrary values and for any W with values whose sums
   are exact (torch's average is then one correctly rounded division by W).
+
+Both the mixed-precision setting (bf16 all-gather, bf16 gradients reduced in
+fp32) and the plain fp32 setting are run; for the former the oracle's fp32
+reduce-scatter wire must also agree.
 """
 
 import os
@@ -34,7 +38,7 @@ def _free_port():
         return s.getsockname()[1]
 
 
-def _oracle_all_gather(plan, xs):
+def _oracle_all_gather(plan, xs, param_dtype="bf16"):
     chunks = []
     for r in range(plan.world_size):
         local = []
@@ -42,19 +46,20 @@ def _oracle_all_gather(plan, xs):
             c = plan.rows_per_rank[p]
             n = O.local_rows(plan, p, r)
             local.append(x[r * c:r * c + n])
-        chunks.append(O.ag_pack(plan, r, local))
+        chunks.append(O.ag_pack(plan, r, local, param_dtype))
     return O.ag_unpack(plan, O.all_gather(chunks))
 
 
-def _oracle_reduce_scatter(plan, grads_by_rank):
-    sends = [O.rs_pack(plan, g) for g in grads_by_rank]
+def _oracle_reduce_scatter(plan, grads_by_rank, reduce_dtype=None):
+    sends = [O.rs_pack(plan, g, reduce_dtype) for g in grads_by_rank]
     return [O.rs_reduce(plan, j, O.rs_exchange(sends, j, plan.chunk)) for j in range(plan.world_size)]
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("w,exact", [(2, False), (3, True), (5, True)])
-def test_oracle_matches_dtensor(tmp_path, w, exact):
-    rng_words = [w, int(exact)]
+@pytest.mark.parametrize("w,exact,mixed", [(2, False, True), (3, True, True), (5, True, True),
+                                           (2, False, False), (3, True, False)])
+def test_oracle_matches_dtensor(tmp_path, w, exact, mixed):
+    rng_words = [w, int(exact), int(mixed)]
     xs = []
     for p, (n, k) in enumerate(DIMS):
         x = random_bits32(rng_words + [p], n * k).view(np.float32).reshape(n, k).copy()
@@ -71,19 +76,27 @@ def test_oracle_matches_dtensor(tmp_path, w, exact):
                 f = np.random.default_rng(rng_words + [r, p]).standard_normal((n, k)) \
                     * np.exp2(np.random.default_rng(rng_words + [r, p, 1]).integers(-20, 21, (n, k)))
                 g = (f.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+            if not mixed:
+                g = O.bf16_to_f32(g).reshape(n, k)         # fp32 gradients with the same values
+                if not exact:
+                    g = g * np.float32(1.0 + 2.0 ** -20)     # use bits below bf16 precision too
             gr.append(g)
-            np.save(tmp_path / f"g_{p}_{r}.npy", g.view(np.int16))
+            np.save(tmp_path / f"g_{p}_{r}.npy", g.view(np.int16) if mixed else g.view(np.int32))
         grads.append(gr)
 
-    mp.spawn(dtensor_worker.run, args=(w, _free_port(), str(tmp_path), len(DIMS)), nprocs=w, join=True)
+    mp.spawn(dtensor_worker.run, args=(w, _free_port(), str(tmp_path), len(DIMS), mixed), nprocs=w, join=True)
 
     plan = O.make_plan(w, DIMS, 8)
-    ag = _oracle_all_gather(plan, xs)
-    rs = _oracle_reduce_scatter(plan, grads)
+    ag = _oracle_all_gather(plan, xs, "bf16" if mixed else "f32")
+    rs_variants = [_oracle_reduce_scatter(plan, grads)]
+    if mixed:
+        rs_variants.append(_oracle_reduce_scatter(plan, grads, "f32"))
     for p in range(len(DIMS)):
         for r in range(w):
-            got = np.load(tmp_path / f"ag_{p}_{r}.npy").view(np.uint16)
-            assert np.array_equal(got, ag[p]), (p, r)
+            got = np.load(tmp_path / f"ag_{p}_{r}.npy")
+            want = ag[p].view(np.uint16) if mixed else ag[p].view(np.uint32)
+            assert np.array_equal(got.view(want.dtype), want), (p, r)
             got_rs = np.load(tmp_path / f"rs_{p}_{r}.npy")
-            assert got_rs.shape == rs[r][p].shape, (p, r)
-            assert np.array_equal(got_rs.view(np.uint32), rs[r][p].view(np.uint32)), (p, r)
+            for rs in rs_variants:
+                assert got_rs.shape == rs[r][p].shape, (p, r)
+                assert np.array_equal(got_rs.view(np.uint32), rs[r][p].view(np.uint32)), (p, r)

@@ -266,3 +266,26 @@ def test_sliced_forms_equal_full_forms(w, dims):
                 v = O.local_elems(plan, p, r)
                 got = O.rs_reduce_range(plan, r, lambda s, c: recv[s:s + c], p, 0, v)
                 assert np.array_equal(got.view(np.uint32), red[p].reshape(-1).view(np.uint32))
+
+
+# ----------------------------------------------------------------- fp32 wires
+
+@pytest.mark.parametrize("w,dims", SMALL_CASES[:6] + [(48, [(86, 1), (100, 3), (1, 8)])])
+def test_fp32_variants(w, dims):
+    impl = oracle_impl()
+    C.check_f32_param_roundtrip(impl, w, dims, seed=w)
+    C.check_f32_wire_same_bits(impl, w, dims, seed=w)
+    C.check_rs_reduce_bruteforce_f32(impl, w, dims, w - 1, seed=w)
+    C.check_rs_reduce_bruteforce_f32(impl, w, dims, 0, seed=w, align=1)
+
+
+def test_fp32_pins_catch_a_rounding_pack():
+    """A pack that rounds to bf16 and widens back when asked for fp32 fails."""
+    impl = oracle_impl()
+
+    def rounding_pack(plan, rank, shards, param_dtype="bf16"):
+        send = O.ag_pack(plan, rank, shards, "bf16")
+        return O.bf16_to_f32(send) if param_dtype == "f32" else send
+    impl.ag_pack = rounding_pack
+    with pytest.raises(AssertionError):
+        C.check_f32_param_roundtrip(impl, 3, [(7, 3), (2, 5)], seed=1)
