@@ -73,6 +73,15 @@ enum {
  * arguments (a Llama block has 9 parameters). */
 #define FSDP_MAX_PARAMS 64
 
+/* World size limit of the chunk-table entry points (*_ex), whose W chunk
+ * pointers also travel in the kernel arguments. */
+#define FSDP_MAX_CHUNKS 128
+
+/* Element types of the *_ex entry points (section 4: param_dtype and
+ * reduce_dtype). */
+typedef int32_t fsdp_dtype;
+enum { FSDP_DTYPE_BF16 = 0, FSDP_DTYPE_F32 = 1 };
+
 typedef struct fsdp_plan fsdp_plan;
 
 /*
@@ -172,6 +181,48 @@ fsdp_status fsdp_rs_pack(const fsdp_plan* plan, const uint16_t* const* grads,
  */
 fsdp_status fsdp_rs_reduce(const fsdp_plan* plan, int32_t rank, const uint16_t* recv,
                            float* const* grad_shards, hipStream_t stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * Element-type and chunk-table forms.
+ *
+ * These generalise the four calls above in two ways:
+ *   - the element type on the wire: param_dtype = fp32 trains without mixed
+ *     precision, and reduce_dtype = fp32 casts the gradients to fp32 before
+ *     the reduce-scatter.  Section 4 makes both dtypes parameters of the
+ *     redistribute; mixed precision is the bf16/fp32 setting.
+ *   - the bucket buffers as W separate chunks.  chunks[i] points at rank i's
+ *     chunk of S elements, so an exchange can be fused with the copy: pull
+ *     the gathered chunks straight from the peers' send chunks, push each
+ *     destination's chunk straight into that peer's receive buffer, and pull
+ *     the W received chunks from the peers' send buffers.
+ * Layouts, zero filling, numerics and error behaviour are those of the
+ * calls above; chunks[] is a host array of W <= FSDP_MAX_CHUNKS device
+ * pointers, each 16-byte aligned.  Errors: as above, plus FSDP_ERR_TOO_MANY
+ * for W > FSDP_MAX_CHUNKS and FSDP_ERR_INVALID for an unknown dtype.
+ * ---------------------------------------------------------------------------
+ */
+
+/* fsdp_ag_pack with param_dtype BF16 (the cast) or F32 (a bit copy of the
+ * fp32 shards).  send_chunk holds S elements of param_dtype. */
+fsdp_status fsdp_ag_pack_ex(const fsdp_plan* plan, int32_t rank, const float* const* shards,
+                            fsdp_dtype param_dtype, void* send_chunk, hipStream_t stream);
+
+/* fsdp_ag_unpack from W chunk pointers (rank i's chunk at chunks[i]); params
+ * and chunks hold param_dtype elements. */
+fsdp_status fsdp_ag_unpack_ex(const fsdp_plan* plan, fsdp_dtype param_dtype, const void* const* chunks,
+                              void* const* params, hipStream_t stream);
+
+/* fsdp_rs_pack into W chunk pointers (destination j's chunk at chunks[j]).
+ * grad_dtype BF16 with reduce_dtype BF16 or F32 (exact widening), or both
+ * F32; F32 gradients on a BF16 wire are refused (FSDP_ERR_INVALID). */
+fsdp_status fsdp_rs_pack_ex(const fsdp_plan* plan, fsdp_dtype grad_dtype, const void* const* grads,
+                            fsdp_dtype reduce_dtype, void* const* chunks, hipStream_t stream);
+
+/* fsdp_rs_reduce from W chunk pointers (source i's chunk at chunks[i]) of
+ * reduce_dtype elements; the sum and division are as in fsdp_rs_reduce. */
+fsdp_status fsdp_rs_reduce_ex(const fsdp_plan* plan, int32_t rank, fsdp_dtype reduce_dtype,
+                              const void* const* chunks, float* const* grad_shards, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -38,9 +38,19 @@ SIGNATURES = {
     "fsdp_ag_unpack": (c_status, [c_plan_p, ctypes.c_void_p, c_ptr_array, ctypes.c_void_p]),
     "fsdp_rs_pack": (c_status, [c_plan_p, c_ptr_array, ctypes.c_void_p, ctypes.c_void_p]),
     "fsdp_rs_reduce": (c_status, [c_plan_p, ctypes.c_int32, ctypes.c_void_p, c_ptr_array, ctypes.c_void_p]),
+    "fsdp_ag_pack_ex": (c_status, [c_plan_p, ctypes.c_int32, c_ptr_array, ctypes.c_int32, ctypes.c_void_p,
+                                   ctypes.c_void_p]),
+    "fsdp_ag_unpack_ex": (c_status, [c_plan_p, ctypes.c_int32, c_ptr_array, c_ptr_array, ctypes.c_void_p]),
+    "fsdp_rs_pack_ex": (c_status, [c_plan_p, ctypes.c_int32, c_ptr_array, ctypes.c_int32, c_ptr_array,
+                                   ctypes.c_void_p]),
+    "fsdp_rs_reduce_ex": (c_status, [c_plan_p, ctypes.c_int32, ctypes.c_int32, c_ptr_array, c_ptr_array,
+                                     ctypes.c_void_p]),
 }
 
 MAX_PARAMS = 64
+MAX_CHUNKS = 128
+DTYPE_BF16 = 0
+DTYPE_F32 = 1
 
 _lib = None
 

@@ -17,6 +17,26 @@ import torch
 from . import _native
 
 BF16_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
+F32_DTYPES = (torch.float32, torch.int32)
+_DTYPE_CODES = {"bf16": 0, "f32": 1}
+
+
+def _dtype_code(name: str) -> int:
+    if name not in _DTYPE_CODES:
+        raise ValueError("dtype must be 'bf16' or 'f32'")
+    return _DTYPE_CODES[name]
+
+
+def _elem_dtypes(name: str):
+    return BF16_DTYPES if name == "bf16" else F32_DTYPES
+
+
+def _dtype_name(t: torch.Tensor) -> str:
+    if t.dtype in BF16_DTYPES:
+        return "bf16"
+    if t.dtype in F32_DTYPES:
+        return "f32"
+    raise TypeError(f"unsupported dtype {t.dtype}")
 
 
 class FsdpError(RuntimeError):
@@ -157,6 +177,58 @@ class BucketPlan:
         arr = _ptr_array(grad_shards, [self.local_elems(p, rank) for p in range(self.num_params)],
                          (torch.float32,), "grad_shards")
         _check(self._lib.fsdp_rs_reduce(self._h, int(rank), src, arr, _stream_handle(stream)), "fsdp_rs_reduce")
+
+    # ---- element-type and chunk-table forms
+    def ag_pack_ex(self, rank: int, shards: Sequence[torch.Tensor], send_chunk: torch.Tensor,
+                   param_dtype: str = "bf16", stream=None) -> None:
+        """fp32 shards -> a chunk of ``param_dtype`` ("bf16" cast or "f32" copy)."""
+        self._check_len(shards, "shards")
+        arr = _ptr_array(shards, [self.local_elems(p, rank) for p in range(self.num_params)],
+                         (torch.float32,), "shards")
+        dst = _bucket_ptr(send_chunk, self.chunk_elems, _elem_dtypes(param_dtype), "send_chunk")
+        _check(self._lib.fsdp_ag_pack_ex(self._h, int(rank), arr, _dtype_code(param_dtype), dst,
+                                         _stream_handle(stream)), "fsdp_ag_pack_ex")
+
+    def ag_unpack_ex(self, chunks: Sequence[torch.Tensor], params: Sequence[torch.Tensor],
+                     param_dtype: str = "bf16", stream=None) -> None:
+        """W gathered chunks (rank i's at chunks[i]) -> full parameters of ``param_dtype``."""
+        self._check_len(params, "params")
+        carr = self._chunk_array(chunks, _elem_dtypes(param_dtype))
+        arr = _ptr_array(params, [self.full_elems(p) for p in range(self.num_params)],
+                         _elem_dtypes(param_dtype), "params")
+        _check(self._lib.fsdp_ag_unpack_ex(self._h, _dtype_code(param_dtype), carr, arr,
+                                           _stream_handle(stream)), "fsdp_ag_unpack_ex")
+
+    def rs_pack_ex(self, grads: Sequence[torch.Tensor], chunks: Sequence[torch.Tensor],
+                   reduce_dtype: str = "bf16", stream=None) -> None:
+        """Full gradients (bf16 or fp32) -> W destination chunks of ``reduce_dtype``."""
+        self._check_len(grads, "grads")
+        names = {_dtype_name(g) for g in grads if g is not None}
+        if len(names) > 1:
+            raise TypeError("all gradients must have one dtype")
+        gname = names.pop() if names else "bf16"
+        arr = _ptr_array(grads, [self.full_elems(p) for p in range(self.num_params)], _elem_dtypes(gname), "grads")
+        carr = self._chunk_array(chunks, _elem_dtypes(reduce_dtype))
+        _check(self._lib.fsdp_rs_pack_ex(self._h, _dtype_code(gname), arr, _dtype_code(reduce_dtype), carr,
+                                         _stream_handle(stream)), "fsdp_rs_pack_ex")
+
+    def rs_reduce_ex(self, rank: int, chunks: Sequence[torch.Tensor], grad_shards: Sequence[torch.Tensor],
+                     reduce_dtype: str = "bf16", stream=None) -> None:
+        """W received chunks (source i's at chunks[i]) of ``reduce_dtype`` -> fp32 shards of ``rank``."""
+        self._check_len(grad_shards, "grad_shards")
+        carr = self._chunk_array(chunks, _elem_dtypes(reduce_dtype))
+        arr = _ptr_array(grad_shards, [self.local_elems(p, rank) for p in range(self.num_params)],
+                         (torch.float32,), "grad_shards")
+        _check(self._lib.fsdp_rs_reduce_ex(self._h, int(rank), _dtype_code(reduce_dtype), carr, arr,
+                                           _stream_handle(stream)), "fsdp_rs_reduce_ex")
+
+    def _chunk_array(self, chunks, dtypes) -> ctypes.Array:
+        if len(chunks) != self.world_size:
+            raise ValueError(f"{len(chunks)} chunks for world size {self.world_size}")
+        arr = (ctypes.c_void_p * len(chunks))()
+        for i, c in enumerate(chunks):
+            arr[i] = _bucket_ptr(c, self.chunk_elems, dtypes, f"chunks[{i}]") or None
+        return arr
 
     # ---- housekeeping
     def _check_len(self, seq, what):

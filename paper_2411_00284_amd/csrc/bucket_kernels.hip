@@ -1,19 +1,24 @@
 // gfx950 kernels and C-ABI entry points of the bucketed FSDP copy path.
 //
-// All four kernels are HBM-bound streams (no contraction, so no MFMA): one
-// launch covers every parameter of a bucket.  The work of a launch is cut
-// into tiles that never cross a parameter (and, for the W-way copies, never
-// cross one rank's segment of a parameter), so that a tile is a plain
-// contiguous copy, cast or reduction with 16-byte vector accesses.  Tiles are
-// numbered parameter by parameter; the first tile of every parameter is kept
-// in one register per lane of a wavefront, and a ballot over it finds the
-// parameter of any tile in O(1).  The per-parameter table travels in the
-// kernel arguments, read through the scalar cache.
+// All kernels are HBM-bound streams (no contraction, so no MFMA): one launch
+// covers every parameter of a bucket.  The work of a launch is cut into tiles
+// that never cross a parameter (and, for the W-way copies, never cross one
+// rank's segment of a parameter), so that a tile is a plain contiguous copy,
+// cast or reduction with 16-byte vector accesses.  Tiles are numbered
+// parameter by parameter; the first tile of every parameter is kept in one
+// register per lane of a wavefront, and a ballot over it finds the parameter
+// of any tile in O(1).  The per-parameter table travels in the kernel
+// arguments, read through the scalar cache.
+//
+// A bucket buffer of W chunks is addressed either as one allocation (chunk i
+// at base + i*stride) or through a table of W chunk pointers, so the same
+// kernels can pull from or push to chunks that live in separate buffers (for
+// an exchange fused with the copy: the chunks of the peers).
 //
 // Numerics (SimpleFSDP sections 3.2.1 and 4):
 //   * fp32 -> bf16 is IEEE round-half-to-even on the 16 dropped bits; NaN
 //     gives (bits >> 16) | 0x0040;
-//   * bf16 -> fp32 is exact (append 16 zero bits);
+//   * bf16 -> fp32 is exact (append 16 zero bits); fp32 copies are bit copies;
 //   * the average is an fp32 sum over source ranks in order 0..W-1, starting
 //     from the rank-0 value, then one IEEE division by W.  The library is
 //     built without fast-math or fp contraction and with fp32 subnormals
@@ -26,6 +31,7 @@
 #include <climits>
 #include <cstdint>
 #include <string>
+#include <type_traits>
 #include <utility>
 #include <vector>
 
@@ -48,6 +54,7 @@ namespace {
 #endif
 
 constexpr int PMAX = FSDP_MAX_PARAMS;
+constexpr int kMaxChunks = FSDP_MAX_CHUNKS;
 constexpr int kReduceBatch = FSDP_REDUCE_BATCH;   // source ranks loaded before they are added
 constexpr int kBlocksPerCU = FSDP_BLOCKS_PER_CU;  // workgroups per CU in the grid-stride launch
 constexpr int kPackGridSlack = 4;                  // max workgroups per tile of work for the 2-D pack grid
@@ -74,11 +81,13 @@ __device__ __forceinline__ int param_of_tile(int my_start, int t) {
     return __builtin_amdgcn_readfirstlane(__popcll(m) - 1);
 }
 
+__device__ __forceinline__ bool is_aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// 16-byte accesses; streamed data may bypass cache retention (non-temporal).
-__device__ __forceinline__ uint4 ld16(const uint16_t* p) {
+// 16-byte accesses; streamed data bypasses cache retention (non-temporal).
+__device__ __forceinline__ uint4 ld16(const void* p) {
     const u32x4* q = reinterpret_cast<const u32x4*>(p);
 #if FSDP_NT_LOAD
     const u32x4 v = __builtin_nontemporal_load(q);
@@ -87,7 +96,7 @@ __device__ __forceinline__ uint4 ld16(const uint16_t* p) {
 #endif
     return make_uint4(v.x, v.y, v.z, v.w);
 }
-__device__ __forceinline__ void st16(uint16_t* p, uint4 v) {
+__device__ __forceinline__ void st16(void* p, uint4 v) {
     u32x4* q = reinterpret_cast<u32x4*>(p);
     const u32x4 w = {v.x, v.y, v.z, v.w};
 #if FSDP_NT_STORE
@@ -115,6 +124,88 @@ __device__ __forceinline__ void stf16(float* p, float4 v) {
 #endif
 }
 
+// ------------------------------------------------------------------ bucket chunk addressing
+
+// One allocation holding W chunks, chunk i at base + i*stride bytes.
+struct ContigChunks {
+    char* base;
+    int64_t stride;
+    __device__ __forceinline__ char* at(int i) const { return base + int64_t(i) * stride; }
+    __device__ __forceinline__ bool aligned() const { return ((uintptr_t(base) | uintptr_t(stride)) & 15) == 0; }
+};
+
+// W chunks anywhere (up to kMaxChunks), chunk i at ptr[i]; the host checks
+// that every chunk is 16-byte aligned.
+struct TableChunks {
+    char* ptr[kMaxChunks];
+    __device__ __forceinline__ char* at(int i) const { return ptr[i]; }
+    __device__ __forceinline__ bool aligned() const { return true; }
+};
+
+// ------------------------------------------------------------------ segment copy
+
+// d[k] = k < v ? s[k] : 0 for k in [lo, hi): one tile of kSteps steps of
+// kCopyBlock threads x 8 elements.  Elements are 2-byte units (bf16, or the
+// halves of fp32 words for a plain copy); kWiden instead reads bf16 and
+// writes fp32.  `vec`: s and d are 16-byte aligned at element 0.
+template <bool kWiden, int kSteps>
+__device__ __forceinline__ void seg_copy(const uint16_t* __restrict__ s, void* __restrict__ dv, int64_t lo,
+                                         int64_t hi, int64_t v, bool vec) {
+    constexpr int64_t kTile = int64_t(kCopyBlock) * kVec * kSteps;
+    uint16_t* __restrict__ d16 = static_cast<uint16_t*>(dv);
+    float* __restrict__ d32 = static_cast<float*>(dv);
+    if (vec && hi - lo == kTile && (hi <= v || lo >= v)) {
+        if (hi <= v) {
+            uint4 x[kSteps];
+#pragma unroll
+            for (int u = 0; u < kSteps; ++u) x[u] = ld16(s + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec);
+#pragma unroll
+            for (int u = 0; u < kSteps; ++u) {
+                const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
+                if (kWiden) {
+                    stf16(d32 + g, make_float4(bf16_lo(x[u].x), bf16_hi(x[u].x), bf16_lo(x[u].y), bf16_hi(x[u].y)));
+                    stf16(d32 + g + 4, make_float4(bf16_lo(x[u].z), bf16_hi(x[u].z), bf16_lo(x[u].w), bf16_hi(x[u].w)));
+                } else {
+                    st16(d16 + g, x[u]);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < kSteps; ++u) {
+                const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
+                if (kWiden) {
+                    stf16(d32 + g, make_float4(0.f, 0.f, 0.f, 0.f));
+                    stf16(d32 + g + 4, make_float4(0.f, 0.f, 0.f, 0.f));
+                } else {
+                    st16(d16 + g, make_uint4(0, 0, 0, 0));
+                }
+            }
+        }
+        return;
+    }
+    for (int u = 0; u < kSteps; ++u) {
+        const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
+        if (g >= hi) break;
+        if (vec && g + kVec <= hi && (g + kVec <= v || g >= v)) {
+            const uint4 x = g < v ? ld16(s + g) : make_uint4(0, 0, 0, 0);
+            if (kWiden) {
+                stf16(d32 + g, make_float4(bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)));
+                stf16(d32 + g + 4, make_float4(bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)));
+            } else {
+                st16(d16 + g, x);
+            }
+            continue;
+        }
+        for (int e = 0; e < kVec; ++e) {
+            const int64_t k = g + e;
+            if (k >= hi) break;
+            const uint16_t x = k < v ? s[k] : uint16_t(0);
+            if (kWiden) d32[k] = bf16_lo(x);
+            else d16[k] = x;
+        }
+    }
+}
+
 // ------------------------------------------------------------------ ag_pack
 
 struct PackArgs {
@@ -122,8 +213,7 @@ struct PackArgs {
     int64_t off[PMAX + 1];       // off[P] = S
     int64_t valid[PMAX];         // n_{p,rank} * inner_p
     int32_t tile_start[PMAX];
-    uint64_t vec_mask;           // bit p: src 16-byte aligned and off_p % 8 == 0
-    uint16_t* dst;
+    void* dst;                   // bf16 or fp32 chunk of S elements
     int32_t nparams;
     int32_t ntiles;
 };
@@ -135,63 +225,82 @@ __device__ __forceinline__ uint4 cast8(const float* __restrict__ s) {
                       bf16x2_bits(b.x, b.y), bf16x2_bits(b.z, b.w));
 }
 
-// Tile lt of parameter p: cast-and-pack its part of [off_p, off_{p+1}).
+// Tile lt of parameter p: its part of [off_p, off_{p+1}) of the chunk, the
+// shard's values cast to bf16 (kCast) or copied as fp32, zeros past the shard.
+template <bool kCast>
 __device__ __forceinline__ void pack_tile(const PackArgs& a, int p, int lt) {
+    typedef typename std::conditional<kCast, uint16_t, uint32_t>::type Out;
     const int64_t off = a.off[p];
     const int64_t region = a.off[p + 1] - off;
     const int64_t valid = a.valid[p];
     const float* __restrict__ src = a.src[p];
-    uint16_t* __restrict__ dst = a.dst + off;
+    Out* __restrict__ dst = static_cast<Out*>(a.dst) + off;
     const int64_t lo = int64_t(lt) * kPackTile;
     const int64_t hi = min(lo + kPackTile, region);
     if (lo >= hi) return;
-    const bool vec = (a.vec_mask >> p) & 1;
+    const bool vec = is_aligned16(src) && is_aligned16(dst);
     if (vec && hi - lo == kPackTile && lo + kPackTile <= valid) {
-        uint4 v[kPackSteps];
 #pragma unroll
-        for (int u = 0; u < kPackSteps; ++u)
-            v[u] = cast8(src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec);
-#pragma unroll
-        for (int u = 0; u < kPackSteps; ++u)
-            st16(dst + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec, v[u]);
+        for (int u = 0; u < kPackSteps; ++u) {
+            const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
+            if (kCast) {
+                st16(dst + g, cast8(src + g));
+            } else {
+                const uint4 x0 = ld16(src + g), x1 = ld16(src + g + 4);
+                st16(dst + g, x0);
+                st16(dst + g + 4, x1);
+            }
+        }
         return;
     }
     for (int u = 0; u < kPackSteps; ++u) {
         const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
         if (g >= hi) break;
         if (vec && g + kVec <= hi && (g + kVec <= valid || g >= valid)) {
-            st16(dst + g, g < valid ? cast8(src + g) : make_uint4(0, 0, 0, 0));
+            if (kCast) {
+                st16(dst + g, g < valid ? cast8(src + g) : make_uint4(0, 0, 0, 0));
+            } else {
+                const uint4 z = make_uint4(0, 0, 0, 0);
+                st16(dst + g, g < valid ? ld16(src + g) : z);
+                st16(dst + g + 4, g < valid ? ld16(src + g + 4) : z);
+            }
             continue;
         }
         for (int e = 0; e < kVec; ++e) {
             const int64_t k = g + e;
-            if (k < hi) dst[k] = k < valid ? uint16_t(bf16_bits(src[k])) : uint16_t(0);
+            if (k >= hi) break;
+            if (kCast) dst[k] = k < valid ? Out(bf16_bits(src[k])) : Out(0);
+            else dst[k] = k < valid ? Out(__float_as_uint(src[k])) : Out(0);
         }
     }
 }
 
 // Tiles numbered across the bucket; the parameter of a tile comes from the
 // wave-ballot lookup.
+template <bool kCast>
 __global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
         const int p = param_of_tile(my_start, t);
-        pack_tile(a, p, t - a.tile_start[p]);
+        pack_tile<kCast>(a, p, t - a.tile_start[p]);
     }
 }
 
 // Grid (x, P): blockIdx.y is the parameter, so a workgroup's first memory
 // access is its data rather than the tile table.  Used when the parameters'
 // tile counts are similar enough that few workgroups find no tile.
+template <bool kCast>
 __global__ void __launch_bounds__(kCopyBlock) ag_pack_grid_kernel(const PackArgs a) {
     const int p = blockIdx.y;
     const int nt = int((a.off[p + 1] - a.off[p] + kPackTile - 1) / kPackTile);
-    for (int lt = blockIdx.x; lt < nt; lt += gridDim.x) pack_tile(a, p, lt);
+    for (int lt = blockIdx.x; lt < nt; lt += gridDim.x) pack_tile<kCast>(a, p, lt);
 }
 
 // ------------------------------------------------------------------ ag_unpack
 
+// Sizes in 2-byte units (an fp32 element is two units).
+template <class Chunks>
 struct UnpackArgs {
     uint16_t* dst[PMAX];
     int64_t off[PMAX];
@@ -199,37 +308,13 @@ struct UnpackArgs {
     int64_t elems[PMAX];         // N_p * inner_p
     int32_t tiles_per_seg[PMAX]; // ceil(L_p / tile)
     int32_t tile_start[PMAX];
-    uint64_t dst_aligned;        // bit p: dst[p] 16-byte aligned
-    const uint16_t* src;         // gathered, rank-major [W][S]
-    int64_t chunk;               // S
+    Chunks src;                  // gathered chunks, one per source rank
     int32_t nparams;
     int32_t ntiles;
 };
 
-// Copy elements [lo, hi) of one segment; `vec` when both ends are 16-byte aligned at 0.
-__device__ __forceinline__ void copy_range(const uint16_t* __restrict__ s, uint16_t* __restrict__ d,
-                                           int64_t lo, int64_t hi, bool vec) {
-    if (vec && hi - lo == kCopyTile) {
-        uint4 v[kCopySteps];
-#pragma unroll
-        for (int u = 0; u < kCopySteps; ++u) v[u] = ld16(s + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec);
-#pragma unroll
-        for (int u = 0; u < kCopySteps; ++u) st16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec, v[u]);
-        return;
-    }
-    for (int u = 0; u < kCopySteps; ++u) {
-        const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
-        if (g >= hi) break;
-        if (vec && g + kVec <= hi) {
-            st16(d + g, ld16(s + g));
-            continue;
-        }
-        for (int e = 0; e < kVec; ++e)
-            if (g + e < hi) d[g + e] = s[g + e];
-    }
-}
-
-__global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs a) {
+template <class Chunks>
+__global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs<Chunks> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
@@ -244,30 +329,31 @@ __global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs 
         const int64_t lo = st * kCopyTile;
         const int64_t hi = min(lo + kCopyTile, v);
         if (lo >= hi) continue;
-        const int64_t soff = int64_t(i) * a.chunk + a.off[p];
-        const int64_t doff = int64_t(i) * L;
-        const bool vec = ((a.dst_aligned >> p) & 1) && ((soff | doff) & (kVec - 1)) == 0;
-        copy_range(a.src + soff, a.dst[p] + doff, lo, hi, vec);
+        const uint16_t* s = reinterpret_cast<const uint16_t*>(a.src.at(i)) + a.off[p];
+        uint16_t* d = a.dst[p] + int64_t(i) * L;
+        seg_copy<false, kCopySteps>(s, d, lo, hi, hi, is_aligned16(s) && is_aligned16(d));
     }
 }
 
 // ------------------------------------------------------------------ rs_pack
 
+// Sizes in units of the source gradient: 2-byte units for a plain copy, bf16
+// elements when kWiden casts them to an fp32 wire.
+template <class Chunks>
 struct RsPackArgs {
-    const uint16_t* src[PMAX];   // full bf16 gradients
+    const uint16_t* src[PMAX];   // full gradients
     int64_t off[PMAX + 1];       // off[P] = S
     int64_t seg[PMAX];
     int64_t elems[PMAX];
     int32_t tiles_per_seg[PMAX]; // ceil((off_{p+1} - off_p) / tile)
     int32_t tile_start[PMAX];
-    uint64_t src_aligned;        // bit p: src[p] 16-byte aligned
-    uint16_t* dst;               // send buffer, destination-major [W][S]
-    int64_t chunk;
+    Chunks dst;                  // send chunks, one per destination rank
     int32_t nparams;
     int32_t ntiles;
 };
 
-__global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs a) {
+template <class Chunks, bool kWiden>
+__global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Chunks> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
@@ -282,46 +368,22 @@ __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs a)
         const int64_t v = rest < L ? (rest > 0 ? rest : 0) : L;
         const int64_t lo = st * kCopyTile;
         const int64_t hi = min(lo + kCopyTile, region);
-        const int64_t doff = int64_t(j) * a.chunk + a.off[p];
-        const int64_t soff = int64_t(j) * L;
-        const uint16_t* __restrict__ s = a.src[p] + soff;
-        uint16_t* __restrict__ d = a.dst + doff;
-        const bool vec = ((a.src_aligned >> p) & 1) && ((soff | doff) & (kVec - 1)) == 0;
-        if (vec && hi - lo == kCopyTile && (hi <= v || lo >= v)) {
-            if (hi <= v) {
-                copy_range(s, d, lo, hi, true);
-            } else {
-#pragma unroll
-                for (int u = 0; u < kCopySteps; ++u)
-                    st16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec, make_uint4(0, 0, 0, 0));
-            }
-            continue;
-        }
-        for (int u = 0; u < kCopySteps; ++u) {
-            const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
-            if (g >= hi) break;
-            if (vec && g + kVec <= hi && (g + kVec <= v || g >= v)) {
-                st16(d + g, g < v ? ld16(s + g) : make_uint4(0, 0, 0, 0));
-                continue;
-            }
-            for (int e = 0; e < kVec; ++e) {
-                const int64_t k = g + e;
-                if (k < hi) d[k] = k < v ? s[k] : uint16_t(0);
-            }
-        }
+        const uint16_t* s = a.src[p] + int64_t(j) * L;
+        void* d = kWiden ? static_cast<void*>(reinterpret_cast<float*>(a.dst.at(j)) + a.off[p])
+                         : static_cast<void*>(reinterpret_cast<uint16_t*>(a.dst.at(j)) + a.off[p]);
+        seg_copy<kWiden, kCopySteps>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
     }
 }
 
 // ------------------------------------------------------------------ rs_reduce
 
+template <class Chunks>
 struct ReduceArgs {
     float* dst[PMAX];
     int64_t off[PMAX];
     int64_t valid[PMAX];         // n_{p,rank} * inner_p
     int32_t tile_start[PMAX];
-    uint64_t dst_aligned;        // bit p: dst[p] 16-byte aligned
-    const uint16_t* src;         // recv, source-major [W][S]
-    int64_t chunk;
+    Chunks src;                  // received chunks, one per source rank
     int32_t world;
     int32_t nparams;
     int32_t ntiles;
@@ -341,101 +403,132 @@ __device__ __forceinline__ void init8(float (&acc)[8], uint4 x) {
     acc[6] = bf16_lo(x.w); acc[7] = bf16_hi(x.w);
 }
 
+// Eight consecutive source values in registers as loaded: bf16 (16 bytes)
+// or fp32 (32 bytes).
+template <typename T> struct Raw8;
+template <> struct Raw8<uint16_t> {
+    uint4 x;
+    __device__ __forceinline__ void load(const uint16_t* p) { x = ld16(p); }
+    __device__ __forceinline__ void init(float (&acc)[8]) const { init8(acc, x); }
+    __device__ __forceinline__ void add(float (&acc)[8]) const { add8(acc, x); }
+};
+template <> struct Raw8<float> {
+    float4 a, b;
+    __device__ __forceinline__ void load(const float* p) { a = ldf16(p); b = ldf16(p + 4); }
+    __device__ __forceinline__ void init(float (&acc)[8]) const {
+        acc[0] = a.x; acc[1] = a.y; acc[2] = a.z; acc[3] = a.w;
+        acc[4] = b.x; acc[5] = b.y; acc[6] = b.z; acc[7] = b.w;
+    }
+    __device__ __forceinline__ void add(float (&acc)[8]) const {
+        acc[0] += a.x; acc[1] += a.y; acc[2] += a.z; acc[3] += a.w;
+        acc[4] += b.x; acc[5] += b.y; acc[6] += b.z; acc[7] += b.w;
+    }
+};
+
 __device__ __forceinline__ void store_avg8(float* d, const float (&acc)[8], float wf) {
     stf16(d, make_float4(acc[0] / wf, acc[1] / wf, acc[2] / wf, acc[3] / wf));
     stf16(d + 4, make_float4(acc[4] / wf, acc[5] / wf, acc[6] / wf, acc[7] / wf));
 }
 
 // Loads of sources i0 .. i0+kReduceBatch-1 (those below W unless kFull) of a
-// full tile; all are issued before any of them is used.
-template <bool kFull>
-__device__ __forceinline__ void load_sources(uint4 (&x)[kReduceBatch][kReduceSteps], const uint16_t* tile,
-                                             int i0, int W, int64_t S, uint32_t t) {
+// full tile; all are issued before any of them is used.  `off` is the tile's
+// element offset inside every chunk.
+template <bool kFull, typename T, class Chunks>
+__device__ __forceinline__ void load_sources(Raw8<T> (&x)[kReduceBatch][kReduceSteps], const Chunks& src,
+                                             int64_t off, int i0, int W, uint32_t t) {
     constexpr uint32_t kStride = uint32_t(kReduceBlock) * kVec;
 #pragma unroll
     for (int b = 0; b < kReduceBatch; ++b) {
         if (kFull || i0 + b < W) {
-            const uint16_t* src = tile + int64_t(i0 + b) * S;
+            const T* s = reinterpret_cast<const T*>(src.at(i0 + b)) + off;
 #pragma unroll
-            for (int u = 0; u < kReduceSteps; ++u) x[b][u] = ld16(src + t + u * kStride);
+            for (int u = 0; u < kReduceSteps; ++u) x[b][u].load(s + t + u * kStride);
         }
     }
 }
 
-// A full tile: kReduceSteps groups of 8 outputs per thread, spaced kReduceBlock*kVec
-// apart.  `tile` is the wave-uniform start of the tile in rank 0's chunk.  The
-// W sources of every output are added in rank order 0..W-1, starting from
-// source 0; the loads of kReduceBatch sources are issued ahead of their adds.
-__device__ __forceinline__ void reduce_tile_vec(const uint16_t* __restrict__ tile, float* __restrict__ dtile,
-                                                int W, int64_t S, float wf) {
+// A full tile: kReduceSteps groups of 8 outputs per thread, spaced
+// kReduceBlock*kVec apart.  The W sources of every output are added in rank
+// order 0..W-1, starting from source 0; the loads of kReduceBatch sources are
+// issued ahead of their adds.
+template <typename T, class Chunks>
+__device__ __forceinline__ void reduce_tile_vec(const Chunks& src, int64_t off, float* __restrict__ dtile,
+                                                int W, float wf) {
     constexpr uint32_t kStride = uint32_t(kReduceBlock) * kVec;
     const uint32_t t = threadIdx.x * kVec;
     float acc[kReduceSteps][8];
-    uint4 x[kReduceBatch][kReduceSteps];
-    if (W >= kReduceBatch) load_sources<true>(x, tile, 0, W, S, t);
-    else load_sources<false>(x, tile, 0, W, S, t);
+    Raw8<T> x[kReduceBatch][kReduceSteps];
+    if (W >= kReduceBatch) load_sources<true>(x, src, off, 0, W, t);
+    else load_sources<false>(x, src, off, 0, W, t);
 #pragma unroll
-    for (int u = 0; u < kReduceSteps; ++u) init8(acc[u], x[0][u]);
+    for (int u = 0; u < kReduceSteps; ++u) x[0][u].init(acc[u]);
 #pragma unroll
     for (int b = 1; b < kReduceBatch; ++b)
         if (b < W) {
 #pragma unroll
-            for (int u = 0; u < kReduceSteps; ++u) add8(acc[u], x[b][u]);
+            for (int u = 0; u < kReduceSteps; ++u) x[b][u].add(acc[u]);
         }
     int i = kReduceBatch;
     for (; i + kReduceBatch <= W; i += kReduceBatch) {
-        load_sources<true>(x, tile, i, W, S, t);
+        load_sources<true>(x, src, off, i, W, t);
 #pragma unroll
         for (int b = 0; b < kReduceBatch; ++b)
 #pragma unroll
-            for (int u = 0; u < kReduceSteps; ++u) add8(acc[u], x[b][u]);
+            for (int u = 0; u < kReduceSteps; ++u) x[b][u].add(acc[u]);
     }
     if (i < W) {
-        load_sources<false>(x, tile, i, W, S, t);
+        load_sources<false>(x, src, off, i, W, t);
 #pragma unroll
         for (int b = 0; b < kReduceBatch; ++b)
             if (i + b < W) {
 #pragma unroll
-                for (int u = 0; u < kReduceSteps; ++u) add8(acc[u], x[b][u]);
+                for (int u = 0; u < kReduceSteps; ++u) x[b][u].add(acc[u]);
             }
     }
 #pragma unroll
     for (int u = 0; u < kReduceSteps; ++u) store_avg8(dtile + t + u * kStride, acc[u], wf);
 }
 
-__global__ void __launch_bounds__(kReduceBlock) rs_reduce_kernel(const ReduceArgs a) {
+__device__ __forceinline__ float widen(uint16_t x) { return bf16_lo(x); }
+__device__ __forceinline__ float widen(float x) { return x; }
+
+template <class Chunks, typename T>
+__global__ void __launch_bounds__(kReduceBlock) rs_reduce_kernel(const ReduceArgs<Chunks> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     const int W = a.world;
     const float wf = float(W);
-    const int64_t S = a.chunk;
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
         const int p = param_of_tile(my_start, t);
         const int64_t v = a.valid[p];
         const int64_t lo = int64_t(t - a.tile_start[p]) * kReduceTile;
-        const uint16_t* __restrict__ s0 = a.src + a.off[p];
+        const int64_t off = a.off[p];
         float* __restrict__ d0 = a.dst[p];
-        const bool vec = ((a.dst_aligned >> p) & 1) && ((a.off[p] | S) & (kVec - 1)) == 0;
+        const bool vec = is_aligned16(d0) && a.src.aligned() && ((off * int64_t(sizeof(T))) & 15) == 0;
         if (vec && lo + kReduceTile <= v) {
-            reduce_tile_vec(s0 + lo, d0 + lo, W, S, wf);
+            reduce_tile_vec<T>(a.src, off + lo, d0 + lo, W, wf);
             continue;
         }
         for (int u = 0; u < kReduceSteps; ++u) {
             const int64_t g = lo + (int64_t(u) * kReduceBlock + threadIdx.x) * kVec;
             if (g >= v) break;
-            const uint16_t* __restrict__ s = s0 + g;
             float* __restrict__ d = d0 + g;
             if (vec && g + kVec <= v) {
                 float acc[8];
-                init8(acc, ld16(s));
-                for (int i = 1; i < W; ++i) add8(acc, ld16(s + int64_t(i) * S));
+                Raw8<T> x;
+                x.load(reinterpret_cast<const T*>(a.src.at(0)) + off + g);
+                x.init(acc);
+                for (int i = 1; i < W; ++i) {
+                    x.load(reinterpret_cast<const T*>(a.src.at(i)) + off + g);
+                    x.add(acc);
+                }
                 store_avg8(d, acc, wf);
                 continue;
             }
             for (int e = 0; e < kVec; ++e) {
                 if (g + e >= v) break;
-                float acc = bf16_lo(s[e]);
-                for (int i = 1; i < W; ++i) acc += bf16_lo(s[int64_t(i) * S + e]);
+                float acc = widen(reinterpret_cast<const T*>(a.src.at(0))[off + g + e]);
+                for (int i = 1; i < W; ++i) acc += widen(reinterpret_cast<const T*>(a.src.at(i))[off + g + e]);
                 d[e] = acc / wf;
             }
         }
@@ -466,10 +559,9 @@ int cu_count(fsdp_status* st) {
 
 struct Span {
     uintptr_t lo, hi;   // [lo, hi) bytes
-    int id;             // -1: the bucket buffer, else the parameter index
 };
 
-bool overlaps(const Span& x, const Span& y) { return x.lo < y.hi && y.lo < x.hi; }
+Span span(const void* p, int64_t bytes) { return {uintptr_t(p), uintptr_t(p) + uintptr_t(bytes)}; }
 
 // Outputs must be pairwise disjoint and disjoint from every input.
 fsdp_status check_overlap(std::vector<Span> outs, const std::vector<Span>& ins) {
@@ -480,15 +572,14 @@ fsdp_status check_overlap(std::vector<Span> outs, const std::vector<Span>& ins) 
         // first output ending after in.lo
         auto it = std::upper_bound(outs.begin(), outs.end(), in.lo,
                                    [](uintptr_t v, const Span& s) { return v < s.hi; });
-        if (it != outs.end() && overlaps(*it, in)) return fail(FSDP_ERR_OVERLAP, "an output overlaps an input");
+        if (it != outs.end() && it->lo < in.hi) return fail(FSDP_ERR_OVERLAP, "an output overlaps an input");
     }
     return FSDP_OK;
 }
 
-fsdp_status check_bucket_ptr(const void* ptr, int64_t elems, const char* name) {
-    if (elems > 0 && ptr == nullptr) return fail(FSDP_ERR_INVALID, std::string(name) + " is NULL");
-    if ((reinterpret_cast<uintptr_t>(ptr) & 15) != 0)
-        return fail(FSDP_ERR_ALIGN, std::string(name) + " is not 16-byte aligned");
+fsdp_status check_bucket_ptr(const void* ptr, int64_t elems, const std::string& name) {
+    if (elems > 0 && ptr == nullptr) return fail(FSDP_ERR_INVALID, name + " is NULL");
+    if ((reinterpret_cast<uintptr_t>(ptr) & 15) != 0) return fail(FSDP_ERR_ALIGN, name + " is not 16-byte aligned");
     return FSDP_OK;
 }
 
@@ -506,41 +597,53 @@ const Plan* get_plan(const fsdp_plan* h, fsdp_status* st) {
     return pl;
 }
 
-bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+bool known_dtype(fsdp_dtype t) { return t == FSDP_DTYPE_BF16 || t == FSDP_DTYPE_F32; }
+int elem_bytes(fsdp_dtype t) { return t == FSDP_DTYPE_F32 ? 4 : 2; }
+
+// A host array of W chunk pointers, each 16-byte aligned and non-NULL when
+// chunks have elements.
+fsdp_status load_chunk_table(const Plan& pl, const void* const* chunks, int esize, TableChunks* out,
+                             std::vector<Span>* spans) {
+    if (chunks == nullptr) return fail(FSDP_ERR_INVALID, "chunks is NULL");
+    if (pl.world > kMaxChunks) return fail(FSDP_ERR_TOO_MANY, "world size exceeds FSDP_MAX_CHUNKS");
+    fsdp_status st;
+    for (int i = 0; i < pl.world; ++i) {
+        if ((st = check_bucket_ptr(chunks[i], pl.chunk, "chunks[" + std::to_string(i) + "]")) != FSDP_OK) return st;
+        out->ptr[i] = static_cast<char*>(const_cast<void*>(chunks[i]));
+        if (pl.chunk > 0) spans->push_back(span(chunks[i], pl.chunk * esize));
+    }
+    return FSDP_OK;
+}
 
 // One launch of `kernel` over `ntiles` work tiles (grid-stride beyond
 // kBlocksPerCU workgroups per CU).  A 2-D launch passes grid.y and the tile
 // count of its x dimension.
 template <typename Args>
 fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream,
-                   dim3 grid2 = dim3(0, 1), int xtiles = 0) {
+                   int grid_y = 1, int xtiles = 0) {
     if (ntiles == 0) return FSDP_OK;
     fsdp_status st = FSDP_OK;
     const int cus = cu_count(&st);
     if (st != FSDP_OK) return st;
-    const dim3 grid = grid2.y > 1 || xtiles > 0
-                          ? dim3(std::min(xtiles, cus * kBlocksPerCU), grid2.y)
-                          : dim3(std::min(ntiles, cus * kBlocksPerCU));
+    const dim3 grid = xtiles > 0 ? dim3(std::min(xtiles, cus * kBlocksPerCU), grid_y)
+                                 : dim3(std::min(ntiles, cus * kBlocksPerCU));
     void* kargs[] = {const_cast<Args*>(&args)};
-    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(block),
-                                         kargs, 0, stream);
+    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(block), kargs, 0, stream);
     if (e != hipSuccess) return fail(FSDP_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
     return FSDP_OK;
 }
 
 int32_t tiles(int64_t n, int64_t tile) { return int32_t((n + tile - 1) / tile); }
 
-}  // namespace
-}  // namespace fsdp
+// ---- ag_pack
 
-using namespace fsdp;
-
-extern "C" fsdp_status fsdp_ag_pack(const fsdp_plan* h, int32_t rank, const float* const* shards,
-                                    uint16_t* send_chunk, hipStream_t stream) {
+fsdp_status do_ag_pack(const fsdp_plan* h, int32_t rank, const float* const* shards, fsdp_dtype wire,
+                       void* send_chunk, hipStream_t stream) {
     clear_error();
     fsdp_status st = FSDP_OK;
     const Plan* pl = get_plan(h, &st);
     if (!pl) return st;
+    if (!known_dtype(wire)) return fail(FSDP_ERR_INVALID, "unknown dtype");
     if (rank < 0 || rank >= pl->world) return fail(FSDP_ERR_INVALID, "rank out of range");
     if (shards == nullptr) return fail(FSDP_ERR_INVALID, "shards is NULL");
     if ((st = check_bucket_ptr(send_chunk, pl->chunk, "send_chunk")) != FSDP_OK) return st;
@@ -554,22 +657,129 @@ extern "C" fsdp_status fsdp_ag_pack(const fsdp_plan* h, int32_t rank, const floa
         a.off[p] = pl->off[p];
         a.valid[p] = v;
         a.tile_start[p] = nt;
-        nt += tiles(pl->off[p + 1] - pl->off[p], kPackTile);
-        max_tiles = std::max(max_tiles, tiles(pl->off[p + 1] - pl->off[p], kPackTile));
-        if (aligned16(shards[p]) && (pl->off[p] & (kVec - 1)) == 0) a.vec_mask |= uint64_t(1) << p;
-        if (v > 0) ins.push_back({uintptr_t(shards[p]), uintptr_t(shards[p] + v), p});
+        const int32_t n = tiles(pl->off[p + 1] - pl->off[p], kPackTile);
+        nt += n;
+        max_tiles = std::max(max_tiles, n);
+        if (v > 0) ins.push_back(span(shards[p], v * 4));
     }
     a.off[pl->nparams] = pl->chunk;
     a.dst = send_chunk;
     a.nparams = pl->nparams;
     a.ntiles = nt;
-    if (pl->chunk > 0 &&
-        (st = check_overlap({{uintptr_t(send_chunk), uintptr_t(send_chunk + pl->chunk), -1}}, ins)) != FSDP_OK)
+    if (pl->chunk > 0 && (st = check_overlap({span(send_chunk, pl->chunk * elem_bytes(wire))}, ins)) != FSDP_OK)
         return st;
     // the 2-D grid launches P * max_tiles workgroups for nt tiles of work
-    if (int64_t(pl->nparams) * max_tiles <= kPackGridSlack * int64_t(nt))
-        return launch(ag_pack_grid_kernel, a, nt, kCopyBlock, stream, dim3(0, pl->nparams), max_tiles);
-    return launch(ag_pack_kernel, a, nt, kCopyBlock, stream);
+    const bool grid2 = int64_t(pl->nparams) * max_tiles <= int64_t(kPackGridSlack) * nt;
+    if (wire == FSDP_DTYPE_BF16)
+        return grid2 ? launch(ag_pack_grid_kernel<true>, a, nt, kCopyBlock, stream, pl->nparams, max_tiles)
+                     : launch(ag_pack_kernel<true>, a, nt, kCopyBlock, stream);
+    return grid2 ? launch(ag_pack_grid_kernel<false>, a, nt, kCopyBlock, stream, pl->nparams, max_tiles)
+                 : launch(ag_pack_kernel<false>, a, nt, kCopyBlock, stream);
+}
+
+// ---- ag_unpack: u = 2-byte units per element
+
+template <class Chunks>
+fsdp_status do_ag_unpack(const Plan& pl, const Chunks& src, const std::vector<Span>& ins, int u,
+                         void* const* params, hipStream_t stream) {
+    fsdp_status st;
+    if (params == nullptr) return fail(FSDP_ERR_INVALID, "params is NULL");
+    UnpackArgs<Chunks> a{};
+    std::vector<Span> outs;
+    int64_t nt = 0;
+    for (int p = 0; p < pl.nparams; ++p) {
+        const int64_t e = pl.elems[p];
+        if ((st = check_param_ptr(params[p], e, 2 * u, p, "params")) != FSDP_OK) return st;
+        a.dst[p] = static_cast<uint16_t*>(params[p]);
+        a.off[p] = pl.off[p] * u;
+        a.seg[p] = pl.seg[p] * u;
+        a.elems[p] = e * u;
+        a.tiles_per_seg[p] = tiles(a.seg[p], kCopyTile);
+        a.tile_start[p] = int32_t(nt);
+        nt += int64_t(pl.world) * a.tiles_per_seg[p];
+        if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
+        if (e > 0) outs.push_back(span(params[p], e * 2 * u));
+    }
+    a.src = src;
+    a.nparams = pl.nparams;
+    a.ntiles = int32_t(nt);
+    if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
+    return launch(ag_unpack_kernel<Chunks>, a, a.ntiles, kCopyBlock, stream);
+}
+
+// ---- rs_pack: gradient elements of `gsize` bytes; kWiden casts bf16 to fp32
+
+template <class Chunks, bool kWiden>
+fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, const Chunks& dst,
+                       const std::vector<Span>& outs, hipStream_t stream) {
+    fsdp_status st;
+    if (grads == nullptr) return fail(FSDP_ERR_INVALID, "grads is NULL");
+    const int u = kWiden ? 1 : gsize / 2;             // kernel units per element
+    RsPackArgs<Chunks> a{};
+    std::vector<Span> ins;
+    int64_t nt = 0;
+    for (int p = 0; p < pl.nparams; ++p) {
+        const int64_t e = pl.elems[p];
+        if ((st = check_param_ptr(grads[p], e, gsize, p, "grads")) != FSDP_OK) return st;
+        a.src[p] = static_cast<const uint16_t*>(grads[p]);
+        a.off[p] = pl.off[p] * u;
+        a.seg[p] = pl.seg[p] * u;
+        a.elems[p] = e * u;
+        a.tiles_per_seg[p] = tiles((pl.off[p + 1] - pl.off[p]) * u, kCopyTile);
+        a.tile_start[p] = int32_t(nt);
+        nt += int64_t(pl.world) * a.tiles_per_seg[p];
+        if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
+        if (e > 0) ins.push_back(span(grads[p], e * gsize));
+    }
+    a.off[pl.nparams] = pl.chunk * u;
+    a.dst = dst;
+    a.nparams = pl.nparams;
+    a.ntiles = int32_t(nt);
+    if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
+    return launch(rs_pack_kernel<Chunks, kWiden>, a, a.ntiles, kCopyBlock, stream);
+}
+
+// ---- rs_reduce: received elements of type T
+
+template <class Chunks, typename T>
+fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const std::vector<Span>& ins,
+                         float* const* grad_shards, hipStream_t stream) {
+    fsdp_status st;
+    if (grad_shards == nullptr) return fail(FSDP_ERR_INVALID, "grad_shards is NULL");
+    ReduceArgs<Chunks> a{};
+    std::vector<Span> outs;
+    int32_t nt = 0;
+    for (int p = 0; p < pl.nparams; ++p) {
+        const int64_t v = pl.local_elems(p, rank);
+        if ((st = check_param_ptr(grad_shards[p], v, 4, p, "grad_shards")) != FSDP_OK) return st;
+        a.dst[p] = grad_shards[p];
+        a.off[p] = pl.off[p];
+        a.valid[p] = v;
+        a.tile_start[p] = nt;
+        nt += tiles(v, kReduceTile);
+        if (v > 0) outs.push_back(span(grad_shards[p], v * 4));
+    }
+    a.src = src;
+    a.world = pl.world;
+    a.nparams = pl.nparams;
+    a.ntiles = nt;
+    if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
+    return launch(rs_reduce_kernel<Chunks, T>, a, nt, kReduceBlock, stream);
+}
+
+}  // namespace
+}  // namespace fsdp
+
+using namespace fsdp;
+
+extern "C" fsdp_status fsdp_ag_pack(const fsdp_plan* h, int32_t rank, const float* const* shards,
+                                    uint16_t* send_chunk, hipStream_t stream) {
+    return do_ag_pack(h, rank, shards, FSDP_DTYPE_BF16, send_chunk, stream);
+}
+
+extern "C" fsdp_status fsdp_ag_pack_ex(const fsdp_plan* h, int32_t rank, const float* const* shards,
+                                       fsdp_dtype param_dtype, void* send_chunk, hipStream_t stream) {
+    return do_ag_pack(h, rank, shards, param_dtype, send_chunk, stream);
 }
 
 extern "C" fsdp_status fsdp_ag_unpack(const fsdp_plan* h, const uint16_t* gathered, uint16_t* const* params,
@@ -578,33 +788,26 @@ extern "C" fsdp_status fsdp_ag_unpack(const fsdp_plan* h, const uint16_t* gather
     fsdp_status st = FSDP_OK;
     const Plan* pl = get_plan(h, &st);
     if (!pl) return st;
-    if (params == nullptr) return fail(FSDP_ERR_INVALID, "params is NULL");
     const int64_t total = int64_t(pl->world) * pl->chunk;
     if ((st = check_bucket_ptr(gathered, total, "gathered")) != FSDP_OK) return st;
-    UnpackArgs a{};
-    std::vector<Span> outs;
-    int32_t nt = 0;
-    for (int p = 0; p < pl->nparams; ++p) {
-        const int64_t e = pl->elems[p];
-        if ((st = check_param_ptr(params[p], e, 2, p, "params")) != FSDP_OK) return st;
-        a.dst[p] = params[p];
-        a.off[p] = pl->off[p];
-        a.seg[p] = pl->seg[p];
-        a.elems[p] = e;
-        a.tiles_per_seg[p] = tiles(pl->seg[p], kCopyTile);
-        a.tile_start[p] = nt;
-        nt += pl->world * a.tiles_per_seg[p];
-        if (aligned16(params[p])) a.dst_aligned |= uint64_t(1) << p;
-        if (e > 0) outs.push_back({uintptr_t(params[p]), uintptr_t(params[p] + e), p});
-    }
-    a.src = gathered;
-    a.chunk = pl->chunk;
-    a.nparams = pl->nparams;
-    a.ntiles = nt;
     std::vector<Span> ins;
-    if (total > 0) ins.push_back({uintptr_t(gathered), uintptr_t(gathered + total), -1});
-    if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    return launch(ag_unpack_kernel, a, nt, kCopyBlock, stream);
+    if (total > 0) ins.push_back(span(gathered, total * 2));
+    const ContigChunks src{reinterpret_cast<char*>(const_cast<uint16_t*>(gathered)), pl->chunk * 2};
+    return do_ag_unpack(*pl, src, ins, 1, reinterpret_cast<void* const*>(params), stream);
+}
+
+extern "C" fsdp_status fsdp_ag_unpack_ex(const fsdp_plan* h, fsdp_dtype param_dtype, const void* const* chunks,
+                                         void* const* params, hipStream_t stream) {
+    clear_error();
+    fsdp_status st = FSDP_OK;
+    const Plan* pl = get_plan(h, &st);
+    if (!pl) return st;
+    if (!known_dtype(param_dtype)) return fail(FSDP_ERR_INVALID, "unknown dtype");
+    const int esize = elem_bytes(param_dtype);
+    TableChunks src{};
+    std::vector<Span> ins;
+    if ((st = load_chunk_table(*pl, chunks, esize, &src, &ins)) != FSDP_OK) return st;
+    return do_ag_unpack(*pl, src, ins, esize / 2, params, stream);
 }
 
 extern "C" fsdp_status fsdp_rs_pack(const fsdp_plan* h, const uint16_t* const* grads, uint16_t* send_buf,
@@ -613,34 +816,29 @@ extern "C" fsdp_status fsdp_rs_pack(const fsdp_plan* h, const uint16_t* const* g
     fsdp_status st = FSDP_OK;
     const Plan* pl = get_plan(h, &st);
     if (!pl) return st;
-    if (grads == nullptr) return fail(FSDP_ERR_INVALID, "grads is NULL");
     const int64_t total = int64_t(pl->world) * pl->chunk;
     if ((st = check_bucket_ptr(send_buf, total, "send_buf")) != FSDP_OK) return st;
-    RsPackArgs a{};
-    std::vector<Span> ins;
-    int32_t nt = 0;
-    for (int p = 0; p < pl->nparams; ++p) {
-        const int64_t e = pl->elems[p];
-        if ((st = check_param_ptr(grads[p], e, 2, p, "grads")) != FSDP_OK) return st;
-        a.src[p] = grads[p];
-        a.off[p] = pl->off[p];
-        a.seg[p] = pl->seg[p];
-        a.elems[p] = e;
-        a.tiles_per_seg[p] = tiles(pl->off[p + 1] - pl->off[p], kCopyTile);
-        a.tile_start[p] = nt;
-        nt += pl->world * a.tiles_per_seg[p];
-        if (aligned16(grads[p])) a.src_aligned |= uint64_t(1) << p;
-        if (e > 0) ins.push_back({uintptr_t(grads[p]), uintptr_t(grads[p] + e), p});
-    }
-    a.off[pl->nparams] = pl->chunk;
-    a.dst = send_buf;
-    a.chunk = pl->chunk;
-    a.nparams = pl->nparams;
-    a.ntiles = nt;
-    if (total > 0 &&
-        (st = check_overlap({{uintptr_t(send_buf), uintptr_t(send_buf + total), -1}}, ins)) != FSDP_OK)
-        return st;
-    return launch(rs_pack_kernel, a, nt, kCopyBlock, stream);
+    std::vector<Span> outs;
+    if (total > 0) outs.push_back(span(send_buf, total * 2));
+    const ContigChunks dst{reinterpret_cast<char*>(send_buf), pl->chunk * 2};
+    return do_rs_pack<ContigChunks, false>(*pl, reinterpret_cast<const void* const*>(grads), 2, dst, outs, stream);
+}
+
+extern "C" fsdp_status fsdp_rs_pack_ex(const fsdp_plan* h, fsdp_dtype grad_dtype, const void* const* grads,
+                                       fsdp_dtype reduce_dtype, void* const* chunks, hipStream_t stream) {
+    clear_error();
+    fsdp_status st = FSDP_OK;
+    const Plan* pl = get_plan(h, &st);
+    if (!pl) return st;
+    if (!known_dtype(grad_dtype) || !known_dtype(reduce_dtype)) return fail(FSDP_ERR_INVALID, "unknown dtype");
+    if (grad_dtype == FSDP_DTYPE_F32 && reduce_dtype == FSDP_DTYPE_BF16)
+        return fail(FSDP_ERR_INVALID, "fp32 gradients on a bf16 wire are not supported");
+    TableChunks dst{};
+    std::vector<Span> outs;
+    if ((st = load_chunk_table(*pl, chunks, elem_bytes(reduce_dtype), &dst, &outs)) != FSDP_OK) return st;
+    if (grad_dtype == FSDP_DTYPE_BF16 && reduce_dtype == FSDP_DTYPE_F32)
+        return do_rs_pack<TableChunks, true>(*pl, grads, 2, dst, outs, stream);
+    return do_rs_pack<TableChunks, false>(*pl, grads, elem_bytes(grad_dtype), dst, outs, stream);
 }
 
 extern "C" fsdp_status fsdp_rs_reduce(const fsdp_plan* h, int32_t rank, const uint16_t* recv,
@@ -650,30 +848,25 @@ extern "C" fsdp_status fsdp_rs_reduce(const fsdp_plan* h, int32_t rank, const ui
     const Plan* pl = get_plan(h, &st);
     if (!pl) return st;
     if (rank < 0 || rank >= pl->world) return fail(FSDP_ERR_INVALID, "rank out of range");
-    if (grad_shards == nullptr) return fail(FSDP_ERR_INVALID, "grad_shards is NULL");
     const int64_t total = int64_t(pl->world) * pl->chunk;
     if ((st = check_bucket_ptr(recv, total, "recv")) != FSDP_OK) return st;
-    ReduceArgs a{};
-    std::vector<Span> outs;
-    int32_t nt = 0;
-    for (int p = 0; p < pl->nparams; ++p) {
-        const int64_t v = pl->local_elems(p, rank);
-        if ((st = check_param_ptr(grad_shards[p], v, 4, p, "grad_shards")) != FSDP_OK) return st;
-        a.dst[p] = grad_shards[p];
-        a.off[p] = pl->off[p];
-        a.valid[p] = v;
-        a.tile_start[p] = nt;
-        nt += tiles(v, kReduceTile);
-        if (aligned16(grad_shards[p])) a.dst_aligned |= uint64_t(1) << p;
-        if (v > 0) outs.push_back({uintptr_t(grad_shards[p]), uintptr_t(grad_shards[p] + v), p});
-    }
-    a.src = recv;
-    a.chunk = pl->chunk;
-    a.world = pl->world;
-    a.nparams = pl->nparams;
-    a.ntiles = nt;
     std::vector<Span> ins;
-    if (total > 0) ins.push_back({uintptr_t(recv), uintptr_t(recv + total), -1});
-    if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    return launch(rs_reduce_kernel, a, nt, kReduceBlock, stream);
+    if (total > 0) ins.push_back(span(recv, total * 2));
+    const ContigChunks src{reinterpret_cast<char*>(const_cast<uint16_t*>(recv)), pl->chunk * 2};
+    return do_rs_reduce<ContigChunks, uint16_t>(*pl, rank, src, ins, grad_shards, stream);
+}
+
+extern "C" fsdp_status fsdp_rs_reduce_ex(const fsdp_plan* h, int32_t rank, fsdp_dtype reduce_dtype,
+                                         const void* const* chunks, float* const* grad_shards, hipStream_t stream) {
+    clear_error();
+    fsdp_status st = FSDP_OK;
+    const Plan* pl = get_plan(h, &st);
+    if (!pl) return st;
+    if (!known_dtype(reduce_dtype)) return fail(FSDP_ERR_INVALID, "unknown dtype");
+    if (rank < 0 || rank >= pl->world) return fail(FSDP_ERR_INVALID, "rank out of range");
+    TableChunks src{};
+    std::vector<Span> ins;
+    if ((st = load_chunk_table(*pl, chunks, elem_bytes(reduce_dtype), &src, &ins)) != FSDP_OK) return st;
+    if (reduce_dtype == FSDP_DTYPE_F32) return do_rs_reduce<TableChunks, float>(*pl, rank, src, ins, grad_shards, stream);
+    return do_rs_reduce<TableChunks, uint16_t>(*pl, rank, src, ins, grad_shards, stream);
 }

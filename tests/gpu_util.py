@@ -99,3 +99,15 @@ def dev_wide_bf16(n: int, seed: int, chunk: int = 1 << 27) -> torch.Tensor:
         bits = torch.where(bits >= 32768, bits - 65536, bits)
         out[s:e] = bits.to(torch.int16)
     return out.view(torch.bfloat16)
+
+
+def dev_wide_f32(n: int, seed: int, chunk: int = 1 << 27) -> torch.Tensor:
+    """n fp32 values N(0,1) * 2^k with k uniform in [-30, 30] (sums round)."""
+    out = torch.empty(n, dtype=torch.float32, device=DEV)
+    g = gen(seed)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        m = e - s
+        k = torch.randint(-30, 31, (m,), dtype=torch.int32, device=DEV, generator=g).to(torch.float32)
+        out[s:e] = torch.randn(m, device=DEV, generator=g) * torch.exp2(k)
+    return out

@@ -232,3 +232,53 @@ def test_binding_checks_tensors():
         BucketPlan(2, [()])
     plan.close()
     plan.close()
+
+
+@no_gpu
+def test_extended_calls_reject_bad_arguments():
+    st_, h = raw_plan(4, [(5, 3), (8, 2)])
+    assert st_ == OK
+    shards = ptrs(FAKE + 4096, FAKE + 8192)
+    chunks = ptrs(*[FAKE + (1 << 20) * (i + 1) for i in range(4)])
+    outs = ptrs(FAKE + (1 << 24), FAKE + (1 << 24) + 4096)
+    # unknown dtypes
+    assert LIB.fsdp_ag_pack_ex(h, 0, shards, 7, FAKE, None) == INVALID
+    assert LIB.fsdp_ag_unpack_ex(h, -1, chunks, outs, None) == INVALID
+    assert LIB.fsdp_rs_pack_ex(h, 0, shards, 2, chunks, None) == INVALID
+    assert LIB.fsdp_rs_reduce_ex(h, 0, 3, chunks, outs, None) == INVALID
+    # fp32 gradients on a bf16 wire
+    assert LIB.fsdp_rs_pack_ex(h, 1, shards, 0, chunks, None) == INVALID
+    # NULL chunk table, NULL or misaligned chunk
+    assert LIB.fsdp_ag_unpack_ex(h, 0, None, outs, None) == INVALID
+    assert LIB.fsdp_rs_reduce_ex(h, 0, 0, ptrs(FAKE, FAKE + 64, None, FAKE + 192), outs, None) == INVALID
+    assert LIB.fsdp_rs_reduce_ex(h, 0, 1, ptrs(FAKE, FAKE + 8, FAKE + 128, FAKE + 192), outs, None) == ALIGN
+    # rank out of range
+    assert LIB.fsdp_rs_reduce_ex(h, 4, 0, chunks, outs, None) == INVALID
+    # output chunks must not overlap each other or the gradients
+    assert LIB.fsdp_rs_pack_ex(h, 0, shards, 0, ptrs(FAKE, FAKE + 16, FAKE + 4096 * 8, FAKE + 4096 * 9),
+                               None) == OVERLAP
+    assert LIB.fsdp_rs_pack_ex(h, 0, ptrs(FAKE + (1 << 20) + 16, FAKE + 8192), 0, chunks, None) == OVERLAP
+    # unpacked parameters must not overlap the chunks they are read from
+    assert LIB.fsdp_ag_unpack_ex(h, 0, chunks, ptrs(FAKE + (1 << 20) + 16, FAKE + (1 << 24)), None) == OVERLAP
+    # fp32 outputs need 4-byte alignment
+    assert LIB.fsdp_ag_unpack_ex(h, 1, chunks, ptrs(FAKE + (1 << 24) + 2, FAKE + (1 << 25)), None) == ALIGN
+    LIB.fsdp_plan_free(h)
+    # more chunks than the table holds
+    st_, h = raw_plan(129, [(300, 2)])
+    assert st_ == OK
+    many = ptrs(*[FAKE + 4096 * i for i in range(129)])
+    assert LIB.fsdp_rs_reduce_ex(h, 0, 0, many, ptrs(FAKE + (1 << 30)), None) == TOO_MANY
+    assert LIB.fsdp_ag_unpack_ex(h, 0, many, ptrs(FAKE + (1 << 30)), None) == TOO_MANY
+    LIB.fsdp_plan_free(h)
+
+
+@no_gpu
+def test_extended_valid_calls_reach_the_runtime():
+    st_, h = raw_plan(2, [(5, 3)])
+    assert st_ == OK
+    chunks = ptrs(FAKE, FAKE + 4096)
+    assert LIB.fsdp_ag_pack_ex(h, 0, ptrs(FAKE + 65536), 1, FAKE, None) == HIP
+    assert LIB.fsdp_ag_unpack_ex(h, 1, chunks, ptrs(FAKE + 65536), None) == HIP
+    assert LIB.fsdp_rs_pack_ex(h, 0, ptrs(FAKE + 65536), 1, chunks, None) == HIP
+    assert LIB.fsdp_rs_reduce_ex(h, 1, 1, chunks, ptrs(FAKE + 65536), None) == HIP
+    LIB.fsdp_plan_free(h)
