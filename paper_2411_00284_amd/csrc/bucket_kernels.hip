@@ -49,6 +49,20 @@ namespace {
 #ifndef FSDP_NT_LOAD
 #define FSDP_NT_LOAD 1
 #endif
+#ifndef FSDP_REDUCE_TAIL_SCALAR
+#define FSDP_REDUCE_TAIL_SCALAR 0
+#endif
+#ifndef FSDP_SADDR
+#define FSDP_SADDR 0
+#endif
+#ifndef FSDP_REDUCE_WAVES
+#define FSDP_REDUCE_WAVES 0
+#endif
+#if FSDP_REDUCE_WAVES
+#define REDUCE_WAVES __attribute__((amdgpu_waves_per_eu(FSDP_REDUCE_WAVES)))
+#else
+#define REDUCE_WAVES
+#endif
 #ifndef FSDP_NT_STORE
 #define FSDP_NT_STORE 1
 #endif
@@ -105,6 +119,26 @@ __device__ __forceinline__ void st16(void* p, uint4 v) {
     *q = w;
 #endif
 }
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint2 ld8(const void* p) {
+    const u32x2* q = reinterpret_cast<const u32x2*>(p);
+#if FSDP_NT_LOAD
+    const u32x2 v = __builtin_nontemporal_load(q);
+#else
+    const u32x2 v = *q;
+#endif
+    return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ void st8(void* p, uint2 v) {
+    u32x2* q = reinterpret_cast<u32x2*>(p);
+    const u32x2 w = {v.x, v.y};
+#if FSDP_NT_STORE
+    __builtin_nontemporal_store(w, q);
+#else
+    *q = w;
+#endif
+}
 __device__ __forceinline__ float4 ldf16(const float* p) {
     const f32x4* q = reinterpret_cast<const f32x4*>(p);
 #if FSDP_NT_LOAD
@@ -134,6 +168,15 @@ struct ContigChunks {
     __device__ __forceinline__ bool aligned() const { return ((uintptr_t(base) | uintptr_t(stride)) & 15) == 0; }
 };
 
+// Contiguous chunks seen as a typed tile pointer plus a stride in elements:
+// chunk i of the tile at tile + i*stride.
+template <typename T>
+struct StridedTile {
+    const T* tile;
+    int64_t stride;
+    __device__ __forceinline__ const T* at(int i) const { return tile + int64_t(i) * stride; }
+};
+
 // W chunks anywhere (up to kMaxChunks), chunk i at ptr[i]; the host checks
 // that every chunk is 16-byte aligned.
 struct TableChunks {
@@ -145,41 +188,23 @@ struct TableChunks {
 // ------------------------------------------------------------------ segment copy
 
 // d[k] = k < v ? s[k] : 0 for k in [lo, hi): one tile of kSteps steps of
-// kCopyBlock threads x 8 elements.  Elements are 2-byte units (bf16, or the
-// halves of fp32 words for a plain copy); kWiden instead reads bf16 and
-// writes fp32.  `vec`: s and d are 16-byte aligned at element 0.
-template <bool kWiden, int kSteps>
-__device__ __forceinline__ void seg_copy(const uint16_t* __restrict__ s, void* __restrict__ dv, int64_t lo,
+// kCopyBlock threads x 8 elements, in 2-byte units (bf16, or the halves of
+// fp32 words for a plain copy).  `vec`: s and d are 16-byte aligned at 0.
+template <int kSteps>
+__device__ __forceinline__ void seg_copy(const uint16_t* __restrict__ s, uint16_t* __restrict__ d, int64_t lo,
                                          int64_t hi, int64_t v, bool vec) {
     constexpr int64_t kTile = int64_t(kCopyBlock) * kVec * kSteps;
-    uint16_t* __restrict__ d16 = static_cast<uint16_t*>(dv);
-    float* __restrict__ d32 = static_cast<float*>(dv);
     if (vec && hi - lo == kTile && (hi <= v || lo >= v)) {
         if (hi <= v) {
             uint4 x[kSteps];
 #pragma unroll
             for (int u = 0; u < kSteps; ++u) x[u] = ld16(s + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec);
 #pragma unroll
-            for (int u = 0; u < kSteps; ++u) {
-                const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
-                if (kWiden) {
-                    stf16(d32 + g, make_float4(bf16_lo(x[u].x), bf16_hi(x[u].x), bf16_lo(x[u].y), bf16_hi(x[u].y)));
-                    stf16(d32 + g + 4, make_float4(bf16_lo(x[u].z), bf16_hi(x[u].z), bf16_lo(x[u].w), bf16_hi(x[u].w)));
-                } else {
-                    st16(d16 + g, x[u]);
-                }
-            }
+            for (int u = 0; u < kSteps; ++u) st16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec, x[u]);
         } else {
 #pragma unroll
-            for (int u = 0; u < kSteps; ++u) {
-                const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
-                if (kWiden) {
-                    stf16(d32 + g, make_float4(0.f, 0.f, 0.f, 0.f));
-                    stf16(d32 + g + 4, make_float4(0.f, 0.f, 0.f, 0.f));
-                } else {
-                    st16(d16 + g, make_uint4(0, 0, 0, 0));
-                }
-            }
+            for (int u = 0; u < kSteps; ++u)
+                st16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec, make_uint4(0, 0, 0, 0));
         }
         return;
     }
@@ -187,21 +212,53 @@ __device__ __forceinline__ void seg_copy(const uint16_t* __restrict__ s, void* _
         const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
         if (g >= hi) break;
         if (vec && g + kVec <= hi && (g + kVec <= v || g >= v)) {
-            const uint4 x = g < v ? ld16(s + g) : make_uint4(0, 0, 0, 0);
-            if (kWiden) {
-                stf16(d32 + g, make_float4(bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)));
-                stf16(d32 + g + 4, make_float4(bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)));
-            } else {
-                st16(d16 + g, x);
-            }
+            st16(d + g, g < v ? ld16(s + g) : make_uint4(0, 0, 0, 0));
             continue;
         }
         for (int e = 0; e < kVec; ++e) {
             const int64_t k = g + e;
             if (k >= hi) break;
-            const uint16_t x = k < v ? s[k] : uint16_t(0);
-            if (kWiden) d32[k] = bf16_lo(x);
-            else d16[k] = x;
+            d[k] = k < v ? s[k] : uint16_t(0);
+        }
+    }
+}
+
+// As seg_copy, but bf16 elements in and their exact fp32 values out.  Each
+// thread handles 4 elements per sub-step (8 bytes in, 16 bytes out), so that
+// every load and store instruction of a wave covers one contiguous run.
+template <int kSteps>
+__device__ __forceinline__ void seg_widen(const uint16_t* __restrict__ s, float* __restrict__ d, int64_t lo,
+                                          int64_t hi, int64_t v, bool vec) {
+    constexpr int kSub = 2 * kSteps;
+    constexpr int64_t kTile = int64_t(kCopyBlock) * 4 * kSub;
+    if (vec && hi - lo == kTile && (hi <= v || lo >= v)) {
+        if (hi <= v) {
+            uint2 x[kSub];
+#pragma unroll
+            for (int u = 0; u < kSub; ++u) x[u] = ld8(s + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4);
+#pragma unroll
+            for (int u = 0; u < kSub; ++u)
+                stf16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4,
+                      make_float4(bf16_lo(x[u].x), bf16_hi(x[u].x), bf16_lo(x[u].y), bf16_hi(x[u].y)));
+        } else {
+#pragma unroll
+            for (int u = 0; u < kSub; ++u)
+                stf16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4, make_float4(0.f, 0.f, 0.f, 0.f));
+        }
+        return;
+    }
+    for (int u = 0; u < kSub; ++u) {
+        const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
+        if (g >= hi) break;
+        if (vec && g + 4 <= hi && (g + 4 <= v || g >= v)) {
+            const uint2 x = g < v ? ld8(s + g) : make_uint2(0, 0);
+            stf16(d + g, make_float4(bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)));
+            continue;
+        }
+        for (int e = 0; e < 4; ++e) {
+            const int64_t k = g + e;
+            if (k >= hi) break;
+            d[k] = k < v ? bf16_lo(s[k]) : 0.f;
         }
     }
 }
@@ -218,18 +275,19 @@ struct PackArgs {
     int32_t ntiles;
 };
 
-__device__ __forceinline__ uint4 cast8(const float* __restrict__ s) {
-    const float4 a = ldf16(s);
-    const float4 b = ldf16(s + 4);
-    return make_uint4(bf16x2_bits(a.x, a.y), bf16x2_bits(a.z, a.w),
-                      bf16x2_bits(b.x, b.y), bf16x2_bits(b.z, b.w));
+// Four fp32 values -> four bf16 bit patterns (8 bytes).
+__device__ __forceinline__ uint2 cast4(float4 a) {
+    return make_uint2(bf16x2_bits(a.x, a.y), bf16x2_bits(a.z, a.w));
 }
 
 // Tile lt of parameter p: its part of [off_p, off_{p+1}) of the chunk, the
 // shard's values cast to bf16 (kCast) or copied as fp32, zeros past the shard.
+// Each thread handles 4 elements per sub-step (16 bytes of fp32 in), so every
+// load and store instruction of a wave covers one contiguous run.
 template <bool kCast>
 __device__ __forceinline__ void pack_tile(const PackArgs& a, int p, int lt) {
     typedef typename std::conditional<kCast, uint16_t, uint32_t>::type Out;
+    constexpr int kSub = 2 * kPackSteps;
     const int64_t off = a.off[p];
     const int64_t region = a.off[p + 1] - off;
     const int64_t valid = a.valid[p];
@@ -240,33 +298,29 @@ __device__ __forceinline__ void pack_tile(const PackArgs& a, int p, int lt) {
     if (lo >= hi) return;
     const bool vec = is_aligned16(src) && is_aligned16(dst);
     if (vec && hi - lo == kPackTile && lo + kPackTile <= valid) {
+        float4 x[kSub];
 #pragma unroll
-        for (int u = 0; u < kPackSteps; ++u) {
-            const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
-            if (kCast) {
-                st16(dst + g, cast8(src + g));
-            } else {
-                const uint4 x0 = ld16(src + g), x1 = ld16(src + g + 4);
-                st16(dst + g, x0);
-                st16(dst + g + 4, x1);
-            }
+        for (int u = 0; u < kSub; ++u) x[u] = ldf16(src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4);
+#pragma unroll
+        for (int u = 0; u < kSub; ++u) {
+            const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
+            if (kCast) st8(dst + g, cast4(x[u]));
+            else stf16(reinterpret_cast<float*>(dst + g), x[u]);
         }
         return;
     }
-    for (int u = 0; u < kPackSteps; ++u) {
-        const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * kVec;
+    for (int u = 0; u < kSub; ++u) {
+        const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
         if (g >= hi) break;
-        if (vec && g + kVec <= hi && (g + kVec <= valid || g >= valid)) {
-            if (kCast) {
-                st16(dst + g, g < valid ? cast8(src + g) : make_uint4(0, 0, 0, 0));
-            } else {
-                const uint4 z = make_uint4(0, 0, 0, 0);
-                st16(dst + g, g < valid ? ld16(src + g) : z);
-                st16(dst + g + 4, g < valid ? ld16(src + g + 4) : z);
-            }
+        if (vec && g + 4 <= hi && (g + 4 <= valid || g >= valid)) {
+            const float4 x = g < valid ? ldf16(src + g) : make_float4(0.f, 0.f, 0.f, 0.f);
+            if (kCast) st8(dst + g, g < valid ? cast4(x) : make_uint2(0, 0));
+            else st16(dst + g, g < valid ? make_uint4(__float_as_uint(x.x), __float_as_uint(x.y),
+                                                      __float_as_uint(x.z), __float_as_uint(x.w))
+                                         : make_uint4(0, 0, 0, 0));
             continue;
         }
-        for (int e = 0; e < kVec; ++e) {
+        for (int e = 0; e < 4; ++e) {
             const int64_t k = g + e;
             if (k >= hi) break;
             if (kCast) dst[k] = k < valid ? Out(bf16_bits(src[k])) : Out(0);
@@ -331,7 +385,7 @@ __global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs<
         if (lo >= hi) continue;
         const uint16_t* s = reinterpret_cast<const uint16_t*>(a.src.at(i)) + a.off[p];
         uint16_t* d = a.dst[p] + int64_t(i) * L;
-        seg_copy<false, kCopySteps>(s, d, lo, hi, hi, is_aligned16(s) && is_aligned16(d));
+        seg_copy<kCopySteps>(s, d, lo, hi, hi, is_aligned16(s) && is_aligned16(d));
     }
 }
 
@@ -369,9 +423,13 @@ __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Ch
         const int64_t lo = st * kCopyTile;
         const int64_t hi = min(lo + kCopyTile, region);
         const uint16_t* s = a.src[p] + int64_t(j) * L;
-        void* d = kWiden ? static_cast<void*>(reinterpret_cast<float*>(a.dst.at(j)) + a.off[p])
-                         : static_cast<void*>(reinterpret_cast<uint16_t*>(a.dst.at(j)) + a.off[p]);
-        seg_copy<kWiden, kCopySteps>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
+        if (kWiden) {
+            float* d = reinterpret_cast<float*>(a.dst.at(j)) + a.off[p];
+            seg_widen<kCopySteps>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
+        } else {
+            uint16_t* d = reinterpret_cast<uint16_t*>(a.dst.at(j)) + a.off[p];
+            seg_copy<kCopySteps>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
+        }
     }
 }
 
@@ -403,18 +461,29 @@ __device__ __forceinline__ void init8(float (&acc)[8], uint4 x) {
     acc[6] = bf16_lo(x.w); acc[7] = bf16_hi(x.w);
 }
 
-// Eight consecutive source values in registers as loaded: bf16 (16 bytes)
-// or fp32 (32 bytes).
+// One thread's 8 values of a tile row (kReduceBlock * 8 elements) of one
+// source, as loaded.  bf16 sources: elements [8t, 8t+8) of the row, one
+// 16-byte load.  fp32 sources: elements [4t, 4t+4) and [4B + 4t, 4B + 4t + 4)
+// (B = kReduceBlock), two 16-byte loads that each cover one contiguous run
+// across the wave.  Addresses are a wave-uniform row pointer plus a 32-bit
+// byte offset.
 template <typename T> struct Raw8;
 template <> struct Raw8<uint16_t> {
     uint4 x;
-    __device__ __forceinline__ void load(const uint16_t* p) { x = ld16(p); }
+    __device__ __forceinline__ static uint32_t pos(uint32_t t, int e) { return t * 8 + e; }
+    __device__ __forceinline__ void load(const uint16_t* row, uint32_t t) { x = ld16(row + t * 8); }
     __device__ __forceinline__ void init(float (&acc)[8]) const { init8(acc, x); }
     __device__ __forceinline__ void add(float (&acc)[8]) const { add8(acc, x); }
 };
 template <> struct Raw8<float> {
     float4 a, b;
-    __device__ __forceinline__ void load(const float* p) { a = ldf16(p); b = ldf16(p + 4); }
+    __device__ __forceinline__ static uint32_t pos(uint32_t t, int e) {
+        return e < 4 ? t * 4 + e : uint32_t(kReduceBlock) * 4 + t * 4 + (e - 4);
+    }
+    __device__ __forceinline__ void load(const float* row, uint32_t t) {
+        a = ldf16(row + t * 4);
+        b = ldf16(row + uint32_t(kReduceBlock) * 4 + t * 4);
+    }
     __device__ __forceinline__ void init(float (&acc)[8]) const {
         acc[0] = a.x; acc[1] = a.y; acc[2] = a.z; acc[3] = a.w;
         acc[4] = b.x; acc[5] = b.y; acc[6] = b.z; acc[7] = b.w;
@@ -425,37 +494,65 @@ template <> struct Raw8<float> {
     }
 };
 
-__device__ __forceinline__ void store_avg8(float* d, const float (&acc)[8], float wf) {
-    stf16(d, make_float4(acc[0] / wf, acc[1] / wf, acc[2] / wf, acc[3] / wf));
-    stf16(d + 4, make_float4(acc[4] / wf, acc[5] / wf, acc[6] / wf, acc[7] / wf));
+// Store the 8 averages of thread t at the positions Raw8<T>::pos gives.
+template <typename T>
+__device__ __forceinline__ void store_avg8(float* row, uint32_t t, const float (&acc)[8], float wf) {
+    const float4 lo = make_float4(acc[0] / wf, acc[1] / wf, acc[2] / wf, acc[3] / wf);
+    const float4 hi = make_float4(acc[4] / wf, acc[5] / wf, acc[6] / wf, acc[7] / wf);
+    stf16(row + Raw8<T>::pos(t, 0), lo);
+    stf16(row + Raw8<T>::pos(t, 4), hi);
 }
 
 // Loads of sources i0 .. i0+kReduceBatch-1 (those below W unless kFull) of a
 // full tile; all are issued before any of them is used.  `off` is the tile's
 // element offset inside every chunk.
-template <bool kFull, typename T, class Chunks>
-__device__ __forceinline__ void load_sources(Raw8<T> (&x)[kReduceBatch][kReduceSteps], const Chunks& src,
+// A wave-uniform pointer, kept in scalar registers.
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+#if FSDP_SADDR
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(v >> 32));
+    // rebuilt as a global-memory pointer, so that loads stay global loads
+    typedef __attribute__((address_space(1))) const char* global_ptr;
+    return (const char*)(global_ptr)((uint64_t(hi) << 32) | lo);
+#else
+    return p;
+#endif
+}
+
+// Typed pointer to the tile of source i: through the chunk table, or as a
+// strided tile of one contiguous buffer.
+template <typename T>
+__device__ __forceinline__ const T* source(const TableChunks& c, int64_t off, int i) {
+    return reinterpret_cast<const T*>(c.at(i)) + off;
+}
+template <typename T>
+__device__ __forceinline__ const T* source(const StridedTile<T>& c, int64_t off, int i) {
+    return c.at(i) + off;
+}
+
+template <bool kFull, typename T, class Src>
+__device__ __forceinline__ void load_sources(Raw8<T> (&x)[kReduceBatch][kReduceSteps], const Src& src,
                                              int64_t off, int i0, int W, uint32_t t) {
-    constexpr uint32_t kStride = uint32_t(kReduceBlock) * kVec;
+    constexpr uint32_t kRow = uint32_t(kReduceBlock) * kVec;
 #pragma unroll
     for (int b = 0; b < kReduceBatch; ++b) {
         if (kFull || i0 + b < W) {
-            const T* s = reinterpret_cast<const T*>(src.at(i0 + b)) + off;
+            const T* s = source<T>(src, off, i0 + b);
 #pragma unroll
-            for (int u = 0; u < kReduceSteps; ++u) x[b][u].load(s + t + u * kStride);
+            for (int u = 0; u < kReduceSteps; ++u) x[b][u].load(s + u * kRow, t);
         }
     }
 }
 
-// A full tile: kReduceSteps groups of 8 outputs per thread, spaced
-// kReduceBlock*kVec apart.  The W sources of every output are added in rank
-// order 0..W-1, starting from source 0; the loads of kReduceBatch sources are
-// issued ahead of their adds.
-template <typename T, class Chunks>
-__device__ __forceinline__ void reduce_tile_vec(const Chunks& src, int64_t off, float* __restrict__ dtile,
+// A full tile of kReduceSteps rows.  The W sources of every output are added
+// in rank order 0..W-1, starting from source 0; the loads of kReduceBatch
+// sources are issued ahead of their adds.
+template <typename T, class Src>
+__device__ __forceinline__ void reduce_tile_vec(const Src& src, int64_t off, float* __restrict__ dtile,
                                                 int W, float wf) {
-    constexpr uint32_t kStride = uint32_t(kReduceBlock) * kVec;
-    const uint32_t t = threadIdx.x * kVec;
+    constexpr uint32_t kRow = uint32_t(kReduceBlock) * kVec;
+    const uint32_t t = threadIdx.x;
     float acc[kReduceSteps][8];
     Raw8<T> x[kReduceBatch][kReduceSteps];
     if (W >= kReduceBatch) load_sources<true>(x, src, off, 0, W, t);
@@ -486,50 +583,106 @@ __device__ __forceinline__ void reduce_tile_vec(const Chunks& src, int64_t off, 
             }
     }
 #pragma unroll
-    for (int u = 0; u < kReduceSteps; ++u) store_avg8(dtile + t + u * kStride, acc[u], wf);
+    for (int u = 0; u < kReduceSteps; ++u) store_avg8<T>(dtile + u * kRow, t, acc[u], wf);
 }
 
 __device__ __forceinline__ float widen(uint16_t x) { return bf16_lo(x); }
 __device__ __forceinline__ float widen(float x) { return x; }
 
+// One thread's group of 8 outputs of one row whose group lies wholly inside
+// the shard (partial tiles): the same rank-ordered sum, loads issued
+// kReduceBatch sources ahead.
+template <typename T, class Src>
+__device__ __forceinline__ void reduce_group_vec(const Src& src, int64_t off, float* __restrict__ drow, int W,
+                                                 float wf, uint32_t t) {
+    float acc[8];
+    Raw8<T> x[kReduceBatch];
+    for (int i = 0; i < W; i += kReduceBatch) {
+#pragma unroll
+        for (int b = 0; b < kReduceBatch; ++b)
+            if (i + b < W) x[b].load(source<T>(src, off, i + b), t);
+#pragma unroll
+        for (int b = 0; b < kReduceBatch; ++b) {
+            if (i + b >= W) break;
+            if (i + b == 0) x[b].init(acc);
+            else x[b].add(acc);
+        }
+    }
+    store_avg8<T>(drow, t, acc, wf);
+}
+
+// One output element at element offset `g` of every chunk (unaligned or
+// ragged parts), loads issued kReduceBatch sources ahead.
+template <typename T, class Src>
+__device__ __forceinline__ float reduce_one(const Src& src, int64_t g, int W, float wf) {
+    float acc = 0.f;
+    T x[kReduceBatch];
+    for (int i = 0; i < W; i += kReduceBatch) {
+#pragma unroll
+        for (int b = 0; b < kReduceBatch; ++b)
+            if (i + b < W) x[b] = source<T>(src, g, i + b)[0];
+#pragma unroll
+        for (int b = 0; b < kReduceBatch; ++b) {
+            if (i + b >= W) break;
+            acc = (i + b == 0) ? widen(x[b]) : acc + widen(x[b]);
+        }
+    }
+    return acc / wf;
+}
+
 template <class Chunks, typename T>
-__global__ void __launch_bounds__(kReduceBlock) rs_reduce_kernel(const ReduceArgs<Chunks> a) {
+__global__ void __launch_bounds__(kReduceBlock) REDUCE_WAVES rs_reduce_kernel(const ReduceArgs<Chunks> a) {
+    constexpr int64_t kRow = int64_t(kReduceBlock) * kVec;
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     const int W = a.world;
     const float wf = float(W);
-    for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
-        const int p = param_of_tile(my_start, t);
+    const uint32_t t = threadIdx.x;
+    for (int tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+        const int p = param_of_tile(my_start, tile);
         const int64_t v = a.valid[p];
-        const int64_t lo = int64_t(t - a.tile_start[p]) * kReduceTile;
+        const int64_t lo = int64_t(tile - a.tile_start[p]) * kReduceTile;
         const int64_t off = a.off[p];
         float* __restrict__ d0 = a.dst[p];
         const bool vec = is_aligned16(d0) && a.src.aligned() && ((off * int64_t(sizeof(T))) & 15) == 0;
         if (vec && lo + kReduceTile <= v) {
-            reduce_tile_vec<T>(a.src, off + lo, d0 + lo, W, wf);
+            if (std::is_same<Chunks, ContigChunks>::value) {
+                const ContigChunks& c = reinterpret_cast<const ContigChunks&>(a.src);
+                const StridedTile<T> st{reinterpret_cast<const T*>(c.base) + off + lo,
+                                        c.stride / int64_t(sizeof(T))};
+                reduce_tile_vec<T>(st, 0, d0 + lo, W, wf);
+            } else {
+                reduce_tile_vec<T>(reinterpret_cast<const TableChunks&>(a.src), off + lo, d0 + lo, W, wf);
+            }
             continue;
         }
+        // partial tile: row by row; a thread's group vectorised when all of it is in range
         for (int u = 0; u < kReduceSteps; ++u) {
-            const int64_t g = lo + (int64_t(u) * kReduceBlock + threadIdx.x) * kVec;
-            if (g >= v) break;
-            float* __restrict__ d = d0 + g;
-            if (vec && g + kVec <= v) {
-                float acc[8];
-                Raw8<T> x;
-                x.load(reinterpret_cast<const T*>(a.src.at(0)) + off + g);
-                x.init(acc);
-                for (int i = 1; i < W; ++i) {
-                    x.load(reinterpret_cast<const T*>(a.src.at(i)) + off + g);
-                    x.add(acc);
+            const int64_t row = lo + u * kRow;
+            if (row >= v) break;
+#if !FSDP_REDUCE_TAIL_SCALAR
+            if (vec && row + Raw8<T>::pos(t, 7) < v) {
+                if (std::is_same<Chunks, ContigChunks>::value) {
+                    const ContigChunks& c = reinterpret_cast<const ContigChunks&>(a.src);
+                    const StridedTile<T> st{reinterpret_cast<const T*>(c.base) + off + row,
+                                            c.stride / int64_t(sizeof(T))};
+                    reduce_group_vec<T>(st, 0, d0 + row, W, wf, t);
+                } else {
+                    reduce_group_vec<T>(reinterpret_cast<const TableChunks&>(a.src), off + row, d0 + row, W, wf, t);
                 }
-                store_avg8(d, acc, wf);
                 continue;
             }
+#endif
             for (int e = 0; e < kVec; ++e) {
-                if (g + e >= v) break;
-                float acc = widen(reinterpret_cast<const T*>(a.src.at(0))[off + g + e]);
-                for (int i = 1; i < W; ++i) acc += widen(reinterpret_cast<const T*>(a.src.at(i))[off + g + e]);
-                d[e] = acc / wf;
+                const int64_t g = row + Raw8<T>::pos(t, e);
+                if (g >= v) continue;
+                if (std::is_same<Chunks, ContigChunks>::value) {
+                    const ContigChunks& c = reinterpret_cast<const ContigChunks&>(a.src);
+                    const StridedTile<T> st{reinterpret_cast<const T*>(c.base), c.stride / int64_t(sizeof(T))};
+                    d0[g] = reduce_one<T>(st, off + g, W, wf);
+                } else {
+                    d0[g] = reduce_one<T>(reinterpret_cast<const TableChunks&>(a.src), off + g, W, wf);
+                }
             }
         }
     }
@@ -746,17 +899,28 @@ fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const 
                          float* const* grad_shards, hipStream_t stream) {
     fsdp_status st;
     if (grad_shards == nullptr) return fail(FSDP_ERR_INVALID, "grad_shards is NULL");
+    // Tiles of the parameters with the fewest tiles are numbered (and so
+    // dispatched) first: a ragged last tile sums its W sources in a longer
+    // dependent chain, which then overlaps the bulk instead of trailing it.
+    std::vector<int> order(pl.nparams);
+    std::vector<int32_t> nts(pl.nparams);
+    for (int p = 0; p < pl.nparams; ++p) {
+        order[p] = p;
+        nts[p] = tiles(pl.local_elems(p, rank), kReduceTile);
+    }
+    std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return nts[x] < nts[y]; });
     ReduceArgs<Chunks> a{};
     std::vector<Span> outs;
     int32_t nt = 0;
-    for (int p = 0; p < pl.nparams; ++p) {
+    for (int q = 0; q < pl.nparams; ++q) {
+        const int p = order[q];
         const int64_t v = pl.local_elems(p, rank);
         if ((st = check_param_ptr(grad_shards[p], v, 4, p, "grad_shards")) != FSDP_OK) return st;
-        a.dst[p] = grad_shards[p];
-        a.off[p] = pl.off[p];
-        a.valid[p] = v;
-        a.tile_start[p] = nt;
-        nt += tiles(v, kReduceTile);
+        a.dst[q] = grad_shards[p];
+        a.off[q] = pl.off[p];
+        a.valid[q] = v;
+        a.tile_start[q] = nt;
+        nt += nts[p];
         if (v > 0) outs.push_back(span(grad_shards[p], v * 4));
     }
     a.src = src;
