@@ -37,7 +37,14 @@ if ROOT not in sys.path:
 METRIC = "effective HBM GB/s (and % of peak) for bucket pack/unpack/reduce"
 PEAK_GBPS = 8000.0                       # MI355X HBM3E
 KERNELS = ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")
-KERNEL_SYMBOLS = {k: f"{k}_kernel" for k in KERNELS}
+# device symbols of the kernels each call launches on a Llama block (ag_pack
+# takes the 2-D grid kernel there); rocprofv3 reports them by these names
+KERNEL_SYMBOLS = {
+    "ag_pack": "ag_pack_grid_kernel<true>",
+    "ag_unpack": "ag_unpack_kernel<ContigChunks>",
+    "rs_pack": "rs_pack_kernel<ContigChunks, false>",
+    "rs_reduce": "rs_reduce_kernel<ContigChunks, unsigned short>",
+}
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_00284_amd", "csrc", "bucket_kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
 
@@ -78,6 +85,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3, help="1 toy, 2 8B, 3 70B (default), 4 405B, 5 uneven")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip timing the fp32-wire and chunk-table forms after the steps")
+    ap.add_argument("--variant-reps", type=int, default=10)
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the steps, run a plain 1 GiB device copy (for counter scaling)")
     args = ap.parse_args(argv)
@@ -171,6 +181,9 @@ def main(argv=None):
         kernels[name] = {"avg_us": round(avg_ms * 1e3, 2), "min_us": round(float(np.min(per_kernel_ms[name])) * 1e3, 2),
                          "bytes": abytes[name], "GBps": round(gbps, 1), "frac": round(gbps / PEAK_GBPS, 4)}
 
+    variants = None if args.no_variants else time_variants(
+        plan, wl, rank, shards, gathered, params, grads, send_buf, recv, outs, stream, args.variant_reps)
+
     if args.copy_probe:
         n = 1 << 29                                # 1 GiB of bf16 read, 1 GiB written
         a = torch.empty(n, dtype=torch.bfloat16, device=dev)
@@ -218,10 +231,63 @@ def main(argv=None):
         "kernels": kernels,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "variants": variants,
     }
     print(json.dumps(line), flush=True)
     plan.close()
     return 0
+
+
+def time_variants(plan, wl, rank, shards, gathered, params, grads, send_buf, recv, outs, stream, reps):
+    """Average launch time of the element-type and chunk-table forms, on the
+    same bucket: fp32 param_dtype pack, W-chunk-table unpack / pack / reduce
+    (tables pointing into the same buffers), bf16 gradients cast to an fp32
+    wire, and the fp32 reduce."""
+    import numpy as np
+    import torch
+
+    W, S = wl.world_size, plan.chunk_elems
+    E = wl.total_elems
+    V0 = sum(plan.local_elems(p, rank) for p in range(wl.num_params))
+    dev = recv.device
+    send_chunk32 = torch.empty(S, dtype=torch.float32, device=dev)
+    send32 = torch.empty(W * S, dtype=torch.float32, device=dev)
+    recv32 = torch.empty(W * S, dtype=torch.float32, device=dev)
+    recv32.copy_(recv)                                  # the same values, widened
+    g_chunks = [gathered[i * S:(i + 1) * S] for i in range(W)]
+    s_chunks = [send_buf[i * S:(i + 1) * S] for i in range(W)]
+    r_chunks = [recv[i * S:(i + 1) * S] for i in range(W)]
+    s32_chunks = [send32[i * S:(i + 1) * S] for i in range(W)]
+    r32_chunks = [recv32[i * S:(i + 1) * S] for i in range(W)]
+    cases = {
+        "ag_pack_f32": (lambda: plan.ag_pack_ex(rank, shards, send_chunk32, "f32", stream), 4 * V0 + 4 * S),
+        "ag_unpack_chunks": (lambda: plan.ag_unpack_ex(g_chunks, params, "bf16", stream), 4 * E),
+        "rs_pack_chunks": (lambda: plan.rs_pack_ex(grads, s_chunks, "bf16", stream), 2 * E + 2 * W * S),
+        "rs_pack_bf16_to_f32": (lambda: plan.rs_pack_ex(grads, s32_chunks, "f32", stream), 2 * E + 4 * W * S),
+        "rs_reduce_chunks": (lambda: plan.rs_reduce_ex(rank, r_chunks, outs, "bf16", stream), 2 * W * V0 + 4 * V0),
+        "rs_reduce_f32": (lambda: plan.rs_reduce_ex(rank, r32_chunks, outs, "f32", stream), 4 * W * V0 + 4 * V0),
+    }
+    flush = torch.empty(1 << 28, dtype=torch.int32, device=dev)   # 1 GiB: evicts L2 and the 256 MB MALL
+    res = {}
+    for name, (fn, nbytes) in cases.items():
+        fn()
+        torch.cuda.synchronize()
+        times = []
+        for k in range(reps):
+            flush.fill_(k)
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            times.append(a.elapsed_time(b))
+        avg_ms = float(np.mean(times))
+        gbps = nbytes / (avg_ms * 1e-3) / 1e9
+        res[name] = {"avg_us": round(avg_ms * 1e3, 2), "bytes": nbytes, "GBps": round(gbps, 1),
+                     "frac": round(gbps / PEAK_GBPS, 4)}
+    del send_chunk32, send32, recv32, flush
+    return res
 
 
 def cpu_baseline(wl, min_seconds=10.0, max_passes=50):
