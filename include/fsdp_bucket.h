@@ -224,6 +224,50 @@ fsdp_status fsdp_rs_pack_ex(const fsdp_plan* plan, fsdp_dtype grad_dtype, const 
 fsdp_status fsdp_rs_reduce_ex(const fsdp_plan* plan, int32_t rank, fsdp_dtype reduce_dtype,
                               const void* const* chunks, float* const* grad_shards, hipStream_t stream);
 
+/*
+ * ---------------------------------------------------------------------------
+ * Auto-wrapping (section 3.3.2 "Auto-wrapping": Algorithm 1, the variables
+ * of Table 1, and the profiling model T_m = alpha + beta * n).  Host code:
+ * no HIP call, no device memory.
+ *
+ * Cuts one pass's all-gather nodes, given in the order the pass computes
+ * them, into consecutive buckets B_0, B_1, ...; step k computes B_k while
+ * the all-gather of B_{k+1} is in flight and, in the backward pass, the
+ * reduce-scatter of B_{k-1}.  Node i joins the bucket being built (B_{k+1})
+ * exactly when
+ *   forward   alpha_ag + beta_ag * (words(B_{k+1}) + ag_words[i]) <= T_c
+ *   backward  T_rs + alpha_ag + beta_ag * (words(B_{k+1}) + ag_words[i]) <= T_c
+ *   and       mem(B_{k+1}) + compute_mem[i] <= mem_max,
+ * where T_c is the sum of compute_time over B_k (0 for the first bucket,
+ * which therefore holds one node unless communication is free), mem() sums
+ * compute_mem, and T_rs = alpha_rs + beta_rs * (rs_words summed over
+ * B_{k-1}), 0 while there is no B_{k-1}.  Otherwise node i starts the next
+ * bucket.  Sums of times run in node order from 0.0 in binary64; each
+ * alpha + beta * n rounds the product and the sum separately.
+ *
+ *   num_nodes     n >= 0
+ *   backward      0 = forward pass, 1 = backward pass
+ *   ag_words      host [n], >= 0: words each node's all-gather moves (n_i)
+ *   rs_words      host [n], >= 0: words of its gradient's reduce-scatter;
+ *                 read in the backward pass only (may be NULL otherwise)
+ *   compute_time  host [n], finite, >= 0: T_ci, in the unit of alpha/beta
+ *   compute_mem   host [n], >= 0: M_ci (e.g. bytes)
+ *   alpha_*, beta_*  finite, >= 0: the collectives' cost model
+ *   mem_max       >= 0: M_max, in the unit of compute_mem
+ *   bucket_of     host [n], out: the bucket number of every node
+ *                 (0-based, non-decreasing, steps of 0 or 1)
+ *   num_buckets   out: the number of buckets (0 when n = 0)
+ * Errors: FSDP_ERR_INVALID for a NULL array, a negative or non-finite
+ * value, or backward not 0/1; FSDP_ERR_OVERFLOW when the words of either
+ * kind sum above 2^53 or the memories overflow int64.  On error no output
+ * is written.  The call keeps no state and is thread-safe.
+ */
+fsdp_status fsdp_auto_wrap(int32_t num_nodes, int32_t backward, const int64_t* ag_words,
+                           const int64_t* rs_words, const double* compute_time,
+                           const int64_t* compute_mem, double alpha_ag, double beta_ag,
+                           double alpha_rs, double beta_rs, int64_t mem_max,
+                           int32_t* bucket_of, int32_t* num_buckets);
+
 #ifdef __cplusplus
 }
 #endif

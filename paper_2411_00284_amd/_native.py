@@ -45,6 +45,11 @@ SIGNATURES = {
                                    ctypes.c_void_p]),
     "fsdp_rs_reduce_ex": (c_status, [c_plan_p, ctypes.c_int32, ctypes.c_int32, c_ptr_array, c_ptr_array,
                                      ctypes.c_void_p]),
+    "fsdp_auto_wrap": (c_status, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
+                                  ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(ctypes.c_int64), ctypes.c_double, ctypes.c_double,
+                                  ctypes.c_double, ctypes.c_double, ctypes.c_int64,
+                                  ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
 }
 
 MAX_PARAMS = 64

@@ -33,7 +33,8 @@ DEVICE_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-command-line-argument",
 ]
-HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-D__HIP_PLATFORM_AMD__"]
+HOST_SOURCES = ["plan.cpp", "auto_wrap.cpp"]
+HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-ffp-contract=off", "-D__HIP_PLATFORM_AMD__"]
 
 
 def _run(cmd, verbose):
@@ -50,11 +51,14 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     inc = [f"-I{INCLUDE}", f"-I{CSRC}", f"-I{os.path.join(ROCM, 'include')}"]
     kobj = os.path.join(BUILD, "bucket_kernels.o")
-    pobj = os.path.join(BUILD, "plan.o")
     _run([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, "bucket_kernels.hip"), "-o", kobj], verbose)
-    _run(["g++", *HOST_FLAGS, *inc, "-c", os.path.join(CSRC, "plan.cpp"), "-o", pobj], verbose)
+    hobjs = []
+    for src in HOST_SOURCES:
+        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+        _run(["g++", *HOST_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
+        hobjs.append(obj)
     tmp = LIB_PATH + f".tmp{os.getpid()}"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, kobj, pobj], verbose)
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, kobj, *hobjs], verbose)
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
 
