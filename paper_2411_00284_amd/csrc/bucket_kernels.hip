@@ -44,24 +44,10 @@ namespace {
 #define FSDP_REDUCE_BATCH 4
 #endif
 #ifndef FSDP_BLOCKS_PER_CU
-#define FSDP_BLOCKS_PER_CU 4096
+#define FSDP_BLOCKS_PER_CU 16384
 #endif
 #ifndef FSDP_NT_LOAD
 #define FSDP_NT_LOAD 1
-#endif
-#ifndef FSDP_REDUCE_TAIL_SCALAR
-#define FSDP_REDUCE_TAIL_SCALAR 0
-#endif
-#ifndef FSDP_SADDR
-#define FSDP_SADDR 0
-#endif
-#ifndef FSDP_REDUCE_WAVES
-#define FSDP_REDUCE_WAVES 0
-#endif
-#if FSDP_REDUCE_WAVES
-#define REDUCE_WAVES __attribute__((amdgpu_waves_per_eu(FSDP_REDUCE_WAVES)))
-#else
-#define REDUCE_WAVES
 #endif
 #ifndef FSDP_NT_STORE
 #define FSDP_NT_STORE 1
@@ -71,7 +57,6 @@ constexpr int PMAX = FSDP_MAX_PARAMS;
 constexpr int kMaxChunks = FSDP_MAX_CHUNKS;
 constexpr int kReduceBatch = FSDP_REDUCE_BATCH;   // source ranks loaded before they are added
 constexpr int kBlocksPerCU = FSDP_BLOCKS_PER_CU;  // workgroups per CU in the grid-stride launch
-constexpr int kPackGridSlack = 4;                  // max workgroups per tile of work for the 2-D pack grid
 
 // ------------------------------------------------------------------ device helpers
 
@@ -229,7 +214,7 @@ __device__ __forceinline__ void seg_copy(const uint16_t* __restrict__ s, uint16_
 template <int kSteps>
 __device__ __forceinline__ void seg_widen(const uint16_t* __restrict__ s, float* __restrict__ d, int64_t lo,
                                           int64_t hi, int64_t v, bool vec) {
-    constexpr int kSub = 2 * kSteps;
+    constexpr int kSub = kSteps;
     constexpr int64_t kTile = int64_t(kCopyBlock) * 4 * kSub;
     if (vec && hi - lo == kTile && (hi <= v || lo >= v)) {
         if (hi <= v) {
@@ -341,16 +326,6 @@ __global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs a) {
     }
 }
 
-// Grid (x, P): blockIdx.y is the parameter, so a workgroup's first memory
-// access is its data rather than the tile table.  Used when the parameters'
-// tile counts are similar enough that few workgroups find no tile.
-template <bool kCast>
-__global__ void __launch_bounds__(kCopyBlock) ag_pack_grid_kernel(const PackArgs a) {
-    const int p = blockIdx.y;
-    const int nt = int((a.off[p + 1] - a.off[p] + kPackTile - 1) / kPackTile);
-    for (int lt = blockIdx.x; lt < nt; lt += gridDim.x) pack_tile<kCast>(a, p, lt);
-}
-
 // ------------------------------------------------------------------ ag_unpack
 
 // Sizes in 2-byte units (an fp32 element is two units).
@@ -420,8 +395,9 @@ __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Ch
         const int64_t L = a.seg[p];
         const int64_t rest = a.elems[p] - int64_t(j) * L;
         const int64_t v = rest < L ? (rest > 0 ? rest : 0) : L;
-        const int64_t lo = st * kCopyTile;
-        const int64_t hi = min(lo + kCopyTile, region);
+        constexpr int64_t kTile = kWiden ? kWidenTile : kCopyTile;
+        const int64_t lo = st * kTile;
+        const int64_t hi = min(lo + kTile, region);
         const uint16_t* s = a.src[p] + int64_t(j) * L;
         if (kWiden) {
             float* d = reinterpret_cast<float*>(a.dst.at(j)) + a.off[p];
@@ -503,23 +479,6 @@ __device__ __forceinline__ void store_avg8(float* row, uint32_t t, const float (
     stf16(row + Raw8<T>::pos(t, 4), hi);
 }
 
-// Loads of sources i0 .. i0+kReduceBatch-1 (those below W unless kFull) of a
-// full tile; all are issued before any of them is used.  `off` is the tile's
-// element offset inside every chunk.
-// A wave-uniform pointer, kept in scalar registers.
-__device__ __forceinline__ const char* uniform_ptr(const char* p) {
-#if FSDP_SADDR
-    const uint64_t v = reinterpret_cast<uint64_t>(p);
-    const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(v));
-    const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(v >> 32));
-    // rebuilt as a global-memory pointer, so that loads stay global loads
-    typedef __attribute__((address_space(1))) const char* global_ptr;
-    return (const char*)(global_ptr)((uint64_t(hi) << 32) | lo);
-#else
-    return p;
-#endif
-}
-
 // Typed pointer to the tile of source i: through the chunk table, or as a
 // strided tile of one contiguous buffer.
 template <typename T>
@@ -531,6 +490,9 @@ __device__ __forceinline__ const T* source(const StridedTile<T>& c, int64_t off,
     return c.at(i) + off;
 }
 
+// Loads of sources i0 .. i0+kReduceBatch-1 (those below W unless kFull) of a
+// full tile; all are issued before any of them is used.  `off` is the tile's
+// element offset inside every chunk.
 template <bool kFull, typename T, class Src>
 __device__ __forceinline__ void load_sources(Raw8<T> (&x)[kReduceBatch][kReduceSteps], const Src& src,
                                              int64_t off, int i0, int W, uint32_t t) {
@@ -631,7 +593,7 @@ __device__ __forceinline__ float reduce_one(const Src& src, int64_t g, int W, fl
 }
 
 template <class Chunks, typename T>
-__global__ void __launch_bounds__(kReduceBlock) REDUCE_WAVES rs_reduce_kernel(const ReduceArgs<Chunks> a) {
+__global__ void __launch_bounds__(kReduceBlock) rs_reduce_kernel(const ReduceArgs<Chunks> a) {
     constexpr int64_t kRow = int64_t(kReduceBlock) * kVec;
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
@@ -660,7 +622,6 @@ __global__ void __launch_bounds__(kReduceBlock) REDUCE_WAVES rs_reduce_kernel(co
         for (int u = 0; u < kReduceSteps; ++u) {
             const int64_t row = lo + u * kRow;
             if (row >= v) break;
-#if !FSDP_REDUCE_TAIL_SCALAR
             if (vec && row + Raw8<T>::pos(t, 7) < v) {
                 if (std::is_same<Chunks, ContigChunks>::value) {
                     const ContigChunks& c = reinterpret_cast<const ContigChunks&>(a.src);
@@ -672,7 +633,6 @@ __global__ void __launch_bounds__(kReduceBlock) REDUCE_WAVES rs_reduce_kernel(co
                 }
                 continue;
             }
-#endif
             for (int e = 0; e < kVec; ++e) {
                 const int64_t g = row + Raw8<T>::pos(t, e);
                 if (g >= v) continue;
@@ -768,18 +728,17 @@ fsdp_status load_chunk_table(const Plan& pl, const void* const* chunks, int esiz
     return FSDP_OK;
 }
 
-// One launch of `kernel` over `ntiles` work tiles (grid-stride beyond
-// kBlocksPerCU workgroups per CU).  A 2-D launch passes grid.y and the tile
-// count of its x dimension.
+// One launch of `kernel` over `ntiles` work tiles, one tile per workgroup up
+// to kBlocksPerCU workgroups per CU (grid-stride beyond that).  The grid also
+// keeps its work-item count below 2^31.
 template <typename Args>
-fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream,
-                   int grid_y = 1, int xtiles = 0) {
+fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream) {
     if (ntiles == 0) return FSDP_OK;
     fsdp_status st = FSDP_OK;
     const int cus = cu_count(&st);
     if (st != FSDP_OK) return st;
-    const dim3 grid = xtiles > 0 ? dim3(std::min(xtiles, cus * kBlocksPerCU), grid_y)
-                                 : dim3(std::min(ntiles, cus * kBlocksPerCU));
+    const int64_t cap = std::min<int64_t>(int64_t(cus) * kBlocksPerCU, (int64_t(1) << 31) / block);
+    const dim3 grid(unsigned(std::min<int64_t>(ntiles, cap)));
     void* kargs[] = {const_cast<Args*>(&args)};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(block), kargs, 0, stream);
     if (e != hipSuccess) return fail(FSDP_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
@@ -802,7 +761,7 @@ fsdp_status do_ag_pack(const fsdp_plan* h, int32_t rank, const float* const* sha
     if ((st = check_bucket_ptr(send_chunk, pl->chunk, "send_chunk")) != FSDP_OK) return st;
     PackArgs a{};
     std::vector<Span> ins;
-    int32_t nt = 0, max_tiles = 0;
+    int32_t nt = 0;
     for (int p = 0; p < pl->nparams; ++p) {
         const int64_t v = pl->local_elems(p, rank);
         if ((st = check_param_ptr(shards[p], v, 4, p, "shards")) != FSDP_OK) return st;
@@ -810,9 +769,7 @@ fsdp_status do_ag_pack(const fsdp_plan* h, int32_t rank, const float* const* sha
         a.off[p] = pl->off[p];
         a.valid[p] = v;
         a.tile_start[p] = nt;
-        const int32_t n = tiles(pl->off[p + 1] - pl->off[p], kPackTile);
-        nt += n;
-        max_tiles = std::max(max_tiles, n);
+        nt += tiles(pl->off[p + 1] - pl->off[p], kPackTile);
         if (v > 0) ins.push_back(span(shards[p], v * 4));
     }
     a.off[pl->nparams] = pl->chunk;
@@ -821,13 +778,8 @@ fsdp_status do_ag_pack(const fsdp_plan* h, int32_t rank, const float* const* sha
     a.ntiles = nt;
     if (pl->chunk > 0 && (st = check_overlap({span(send_chunk, pl->chunk * elem_bytes(wire))}, ins)) != FSDP_OK)
         return st;
-    // the 2-D grid launches P * max_tiles workgroups for nt tiles of work
-    const bool grid2 = int64_t(pl->nparams) * max_tiles <= int64_t(kPackGridSlack) * nt;
-    if (wire == FSDP_DTYPE_BF16)
-        return grid2 ? launch(ag_pack_grid_kernel<true>, a, nt, kCopyBlock, stream, pl->nparams, max_tiles)
-                     : launch(ag_pack_kernel<true>, a, nt, kCopyBlock, stream);
-    return grid2 ? launch(ag_pack_grid_kernel<false>, a, nt, kCopyBlock, stream, pl->nparams, max_tiles)
-                 : launch(ag_pack_kernel<false>, a, nt, kCopyBlock, stream);
+    if (wire == FSDP_DTYPE_BF16) return launch(ag_pack_kernel<true>, a, nt, kCopyBlock, stream);
+    return launch(ag_pack_kernel<false>, a, nt, kCopyBlock, stream);
 }
 
 // ---- ag_unpack: u = 2-byte units per element
@@ -878,7 +830,7 @@ fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, cons
         a.off[p] = pl.off[p] * u;
         a.seg[p] = pl.seg[p] * u;
         a.elems[p] = e * u;
-        a.tiles_per_seg[p] = tiles((pl.off[p + 1] - pl.off[p]) * u, kCopyTile);
+        a.tiles_per_seg[p] = tiles((pl.off[p + 1] - pl.off[p]) * u, kWiden ? kWidenTile : kCopyTile);
         a.tile_start[p] = int32_t(nt);
         nt += int64_t(pl.world) * a.tiles_per_seg[p];
         if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");

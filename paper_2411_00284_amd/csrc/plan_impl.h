@@ -33,6 +33,9 @@ constexpr int kVec = 8;
 constexpr int kCopyBlock = FSDP_COPY_BLOCK;
 constexpr int kCopySteps = FSDP_COPY_STEPS;
 constexpr int64_t kCopyTile = int64_t(kCopyBlock) * kVec * kCopySteps;
+// The widening pack (bf16 in, fp32 out) moves 4 elements per thread and step,
+// so its tiles read half and write the same bytes as a copy tile.
+constexpr int64_t kWidenTile = int64_t(kCopyBlock) * 4 * kCopySteps;
 constexpr int kPackSteps = FSDP_PACK_STEPS;
 constexpr int64_t kPackTile = int64_t(kCopyBlock) * kVec * kPackSteps;
 constexpr int kReduceBlock = FSDP_REDUCE_BLOCK;
