@@ -544,6 +544,24 @@ __device__ __forceinline__ void reduce_tile_vec(const Src& src, int64_t off, flo
                 for (int u = 0; u < kReduceSteps; ++u) x[b][u].add(acc[u]);
             }
     }
+    if constexpr (std::is_same<T, uint16_t>::value) {
+        // Thread t holds outputs [8t, 8t + 8) of each row: staged through LDS
+        // so that every store instruction of a wave covers one contiguous run.
+        __shared__ float4 stage[kReduceSteps * kReduceBlock * 2];
+#pragma unroll
+        for (int u = 0; u < kReduceSteps; ++u) {
+            stage[(u * kReduceBlock + t) * 2] = make_float4(acc[u][0] / wf, acc[u][1] / wf, acc[u][2] / wf, acc[u][3] / wf);
+            stage[(u * kReduceBlock + t) * 2 + 1] = make_float4(acc[u][4] / wf, acc[u][5] / wf, acc[u][6] / wf, acc[u][7] / wf);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kReduceSteps; ++u)
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                stf16(dtile + u * kRow + (h * kReduceBlock + t) * 4, stage[u * kReduceBlock * 2 + h * kReduceBlock + t]);
+        __syncthreads();
+        return;
+    }
 #pragma unroll
     for (int u = 0; u < kReduceSteps; ++u) store_avg8<T>(dtile + u * kRow, t, acc[u], wf);
 }
