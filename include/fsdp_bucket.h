@@ -45,6 +45,10 @@
  *     returns (kernel arguments are copied at launch); plans are immutable
  *     and may be shared between threads and streams.
  *   - bf16 values are passed as uint16_t bit patterns.
+ *   - A launch uses one workgroup per work tile, up to a per-device cap;
+ *     past the cap every workgroup loops over several tiles.  The
+ *     environment variable FSDP_MAX_WORKGROUPS, when it holds a positive
+ *     count, lowers that cap (read at every launch; results do not change).
  */
 #ifndef FSDP_BUCKET_H
 #define FSDP_BUCKET_H

@@ -29,6 +29,7 @@
 #include <algorithm>
 #include <atomic>
 #include <climits>
+#include <cstdlib>
 #include <cstdint>
 #include <string>
 #include <type_traits>
@@ -748,14 +749,19 @@ fsdp_status load_chunk_table(const Plan& pl, const void* const* chunks, int esiz
 
 // One launch of `kernel` over `ntiles` work tiles, one tile per workgroup up
 // to kBlocksPerCU workgroups per CU (grid-stride beyond that).  The grid also
-// keeps its work-item count below 2^31.
+// keeps its work-item count below 2^31, and below FSDP_MAX_WORKGROUPS when
+// that environment variable holds a positive count.
 template <typename Args>
 fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream) {
     if (ntiles == 0) return FSDP_OK;
     fsdp_status st = FSDP_OK;
     const int cus = cu_count(&st);
     if (st != FSDP_OK) return st;
-    const int64_t cap = std::min<int64_t>(int64_t(cus) * kBlocksPerCU, (int64_t(1) << 31) / block);
+    int64_t cap = std::min<int64_t>(int64_t(cus) * kBlocksPerCU, (int64_t(1) << 31) / block);
+    if (const char* env = std::getenv("FSDP_MAX_WORKGROUPS")) {
+        const long long m = std::atoll(env);
+        if (m > 0) cap = std::min<int64_t>(cap, m);
+    }
     const dim3 grid(unsigned(std::min<int64_t>(ntiles, cap)));
     void* kargs[] = {const_cast<Args*>(&args)};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(block), kargs, 0, stream);

@@ -123,6 +123,26 @@ def wide_bf16_host(words, n):
 
 # ----------------------------------------------------------------- small buckets
 
+@pytest.mark.parametrize("cap", [1, 3, 50])
+@pytest.mark.parametrize("case", [3, 8, 10, 11])
+def test_grid_stride(case, cap, monkeypatch):
+    """With the workgroup cap lowered, every workgroup loops over many tiles
+    (of several parameters, and through the reduce's LDS staging more than
+    once); the results stay bit-exact."""
+    monkeypatch.setenv("FSDP_MAX_WORKGROUPS", str(cap))
+    w, dims = SMALL[case]
+    plan = BucketPlan(w, dims, 8)
+    oplan = O.make_plan(w, dims, 8)
+    for r in _ranks(w):
+        run_ag_pack(plan, oplan, r, seed=case)
+    run_ag_unpack(plan, oplan, seed=case)
+    run_rs_pack(plan, oplan, seed=case)
+    recv = wide_bf16_host([case, cap], w * oplan.chunk)
+    for r in _ranks(w):
+        run_rs_reduce(plan, oplan, r, recv)
+    plan.close()
+
+
 @pytest.mark.parametrize("case", range(len(SMALL)))
 @pytest.mark.parametrize("align", [8, 1])
 def test_small_buckets(case, align):

@@ -144,6 +144,14 @@ def test_ex_small(case, align):
     plan.close()
 
 
+@pytest.mark.parametrize("cap", [1, 7])
+def test_ex_grid_stride(cap, monkeypatch):
+    """The element-type and chunk-table forms with every workgroup looping over
+    many tiles."""
+    monkeypatch.setenv("FSDP_MAX_WORKGROUPS", str(cap))
+    test_ex_small(5, 8)
+
+
 def test_ex_chunks_alias_one_buffer():
     """The chunk table may point into one [W][S] buffer: the results equal the
     contiguous calls bit for bit."""
