@@ -241,6 +241,7 @@ def main(argv=None):
         "roofline": roofline,
         "cpu_baseline": cpu,
         "variants": variants,
+        "auto_wrap": None if args.no_variants else time_auto_wrap(wl),
     }
     print(json.dumps(line), flush=True)
     plan.close()
@@ -296,6 +297,36 @@ def time_variants(plan, wl, rank, shards, gathered, params, grads, send_buf, rec
         res[name] = {"avg_us": round(avg_ms * 1e3, 2), "bytes": nbytes, "GBps": round(gbps, 1),
                      "frac": round(gbps / PEAK_GBPS, 4)}
     del send_chunk32, send32, recv32, flush
+    return res
+
+
+def time_auto_wrap(wl, layers=80, reps=20):
+    """Host time of the library's auto-wrapping planner (fsdp_auto_wrap) on a
+    whole-model pass: ``layers`` copies of the workload's block, one node per
+    parameter.  Node words are the padded all-gather sizes at the workload's W;
+    compute times and memories are a synthetic scale (2 flop per weight and
+    token over 65536 tokens at 2.5 PFLOP/s; bf16 weights plus a fixed
+    activation share), and the collectives cost 20 us + 2 bytes / 100 GB/s per
+    word.  Only the planner is timed (binding included)."""
+    import numpy as np
+
+    from paper_2411_00284_amd import auto_wrap
+
+    W = wl.world_size
+    ag, t, m = [], [], []
+    for _ in range(layers):
+        for n, k in wl.dims:
+            ag.append(W * (-(-n // W)) * k)
+            t.append(2.0 * n * k * 65536 / 2.5e15)
+            m.append(2 * n * k + (1 << 24))
+    res = {"nodes": len(ag)}
+    for name, backward in (("forward", False), ("backward", True)):
+        times = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            buckets = auto_wrap(ag, t, m, 20e-6, 2 / 100e9, 8 << 30, backward, ag, 20e-6, 2 / 100e9)
+            times.append(time.perf_counter() - t0)
+        res[name] = {"buckets": len(buckets), "us_per_pass": round(float(np.median(times)) * 1e6, 1)}
     return res
 
 
