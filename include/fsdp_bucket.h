@@ -181,7 +181,8 @@ fsdp_status fsdp_rs_pack(const fsdp_plan* plan, const uint16_t* const* grads,
  *                a = x_0; a = fl32(a + x_i) for i = 1..W-1; out = fl32(a / W)
  *                with x_i = recv[i*S + off_p + k] widened exactly to fp32,
  *                additions in rank order, a correctly rounded division and
- *                subnormals kept.
+ *                subnormals kept.  A NaN among the x_i gives a NaN output;
+ *                which NaN (its payload) is left open, as IEEE 754 leaves it.
  */
 fsdp_status fsdp_rs_reduce(const fsdp_plan* plan, int32_t rank, const uint16_t* recv,
                            float* const* grad_shards, hipStream_t stream);
