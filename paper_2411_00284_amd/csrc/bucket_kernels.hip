@@ -753,7 +753,7 @@ fsdp_status load_chunk_table(const Plan& pl, const void* const* chunks, int esiz
 // that environment variable holds a positive count.
 template <typename Args>
 fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream) {
-    if (ntiles == 0) return FSDP_OK;
+    if (ntiles <= 0) return FSDP_OK;
     fsdp_status st = FSDP_OK;
     const int cus = cu_count(&st);
     if (st != FSDP_OK) return st;
@@ -769,7 +769,7 @@ fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int
     return FSDP_OK;
 }
 
-int32_t tiles(int64_t n, int64_t tile) { return int32_t((n + tile - 1) / tile); }
+int64_t tiles(int64_t n, int64_t tile) { return (n + tile - 1) / tile; }
 
 // ---- ag_pack
 
@@ -785,25 +785,26 @@ fsdp_status do_ag_pack(const fsdp_plan* h, int32_t rank, const float* const* sha
     if ((st = check_bucket_ptr(send_chunk, pl->chunk, "send_chunk")) != FSDP_OK) return st;
     PackArgs a{};
     std::vector<Span> ins;
-    int32_t nt = 0;
+    int64_t nt = 0;   // at most the planner's checked pack tile count
     for (int p = 0; p < pl->nparams; ++p) {
         const int64_t v = pl->local_elems(p, rank);
         if ((st = check_param_ptr(shards[p], v, 4, p, "shards")) != FSDP_OK) return st;
         a.src[p] = shards[p];
         a.off[p] = pl->off[p];
         a.valid[p] = v;
-        a.tile_start[p] = nt;
+        a.tile_start[p] = int32_t(nt);
         nt += tiles(pl->off[p + 1] - pl->off[p], kPackTile);
         if (v > 0) ins.push_back(span(shards[p], v * 4));
     }
     a.off[pl->nparams] = pl->chunk;
     a.dst = send_chunk;
     a.nparams = pl->nparams;
-    a.ntiles = nt;
+    if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
+    a.ntiles = int32_t(nt);
     if (pl->chunk > 0 && (st = check_overlap({span(send_chunk, pl->chunk * elem_bytes(wire))}, ins)) != FSDP_OK)
         return st;
-    if (wire == FSDP_DTYPE_BF16) return launch(ag_pack_kernel<true>, a, nt, kCopyBlock, stream);
-    return launch(ag_pack_kernel<false>, a, nt, kCopyBlock, stream);
+    if (wire == FSDP_DTYPE_BF16) return launch(ag_pack_kernel<true>, a, a.ntiles, kCopyBlock, stream);
+    return launch(ag_pack_kernel<false>, a, a.ntiles, kCopyBlock, stream);
 }
 
 // ---- ag_unpack: u = 2-byte units per element
@@ -823,7 +824,9 @@ fsdp_status do_ag_unpack(const Plan& pl, const Chunks& src, const std::vector<Sp
         a.off[p] = pl.off[p] * u;
         a.seg[p] = pl.seg[p] * u;
         a.elems[p] = e * u;
-        a.tiles_per_seg[p] = tiles(a.seg[p], kCopyTile);
+        const int64_t tps = tiles(a.seg[p], kCopyTile);
+        if (tps > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
+        a.tiles_per_seg[p] = int32_t(tps);
         a.tile_start[p] = int32_t(nt);
         nt += int64_t(pl.world) * a.tiles_per_seg[p];
         if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
@@ -854,7 +857,9 @@ fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, cons
         a.off[p] = pl.off[p] * u;
         a.seg[p] = pl.seg[p] * u;
         a.elems[p] = e * u;
-        a.tiles_per_seg[p] = tiles((pl.off[p + 1] - pl.off[p]) * u, kWiden ? kWidenTile : kCopyTile);
+        const int64_t tps = tiles((pl.off[p + 1] - pl.off[p]) * u, kWiden ? kWidenTile : kCopyTile);
+        if (tps > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
+        a.tiles_per_seg[p] = int32_t(tps);
         a.tile_start[p] = int32_t(nt);
         nt += int64_t(pl.world) * a.tiles_per_seg[p];
         if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
@@ -879,7 +884,7 @@ fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const 
     // dispatched) first: a ragged last tile sums its W sources in a longer
     // dependent chain, which then overlaps the bulk instead of trailing it.
     std::vector<int> order(pl.nparams);
-    std::vector<int32_t> nts(pl.nparams);
+    std::vector<int64_t> nts(pl.nparams);
     for (int p = 0; p < pl.nparams; ++p) {
         order[p] = p;
         nts[p] = tiles(pl.local_elems(p, rank), kReduceTile);
@@ -887,7 +892,7 @@ fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const 
     std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return nts[x] < nts[y]; });
     ReduceArgs<Chunks> a{};
     std::vector<Span> outs;
-    int32_t nt = 0;
+    int64_t nt = 0;   // at most the planner's checked reduce tile count
     for (int q = 0; q < pl.nparams; ++q) {
         const int p = order[q];
         const int64_t v = pl.local_elems(p, rank);
@@ -895,16 +900,17 @@ fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const 
         a.dst[q] = grad_shards[p];
         a.off[q] = pl.off[p];
         a.valid[q] = v;
-        a.tile_start[q] = nt;
+        a.tile_start[q] = int32_t(nt);
         nt += nts[p];
         if (v > 0) outs.push_back(span(grad_shards[p], v * 4));
     }
     a.src = src;
     a.world = pl.world;
     a.nparams = pl.nparams;
-    a.ntiles = nt;
+    if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
+    a.ntiles = int32_t(nt);
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    return launch(rs_reduce_kernel<Chunks, T>, a, nt, kReduceBlock, stream);
+    return launch(rs_reduce_kernel<Chunks, T>, a, a.ntiles, kReduceBlock, stream);
 }
 
 }  // namespace

@@ -282,3 +282,17 @@ def test_extended_valid_calls_reach_the_runtime():
     assert LIB.fsdp_rs_pack_ex(h, 0, ptrs(FAKE + 65536), 1, chunks, None) == HIP
     assert LIB.fsdp_rs_reduce_ex(h, 1, 1, chunks, ptrs(FAKE + 65536), None) == HIP
     LIB.fsdp_plan_free(h)
+
+
+@no_gpu
+def test_widening_pack_tile_count_overflow():
+    """A bucket the planner accepts can still need more than 2^31 - 1 work tiles
+    for the widening pack (half-size tiles): the call fails with
+    FSDP_ERR_OVERFLOW before any HIP call."""
+    n = 2 * ((1 << 40) + 8)
+    st_, h = raw_plan(2, [(n, 1)])
+    assert st_ == OK
+    chunks = ptrs(FAKE, FAKE + (1 << 44))
+    assert LIB.fsdp_rs_pack_ex(h, 0, ptrs(FAKE + (1 << 46)), 1, chunks, None) == OVERFLOW
+    assert b"tiles" in LIB.fsdp_last_error()
+    LIB.fsdp_plan_free(h)
