@@ -250,7 +250,8 @@ def main(argv=None):
 
 def time_variants(plan, wl, rank, shards, gathered, params, grads, send_buf, recv, outs, stream, reps):
     """Average launch time of the element-type and chunk-table forms, on the
-    same bucket: fp32 param_dtype pack, W-chunk-table unpack / pack / reduce
+    same bucket: fp32 param_dtype pack, the pack pushed to W chunks,
+    W-chunk-table unpack / pack / reduce
     (tables pointing into the same buffers), bf16 gradients cast to an fp32
     wire, and the fp32 reduce."""
     import numpy as np
@@ -271,6 +272,7 @@ def time_variants(plan, wl, rank, shards, gathered, params, grads, send_buf, rec
     r32_chunks = [recv32[i * S:(i + 1) * S] for i in range(W)]
     cases = {
         "ag_pack_f32": (lambda: plan.ag_pack_ex(rank, shards, send_chunk32, "f32", stream), 4 * V0 + 4 * S),
+        "ag_pack_push": (lambda: plan.ag_pack_push(rank, shards, s_chunks, "bf16", stream), 4 * V0 + 2 * W * S),
         "ag_unpack_chunks": (lambda: plan.ag_unpack_ex(g_chunks, params, "bf16", stream), 4 * E),
         "rs_pack_chunks": (lambda: plan.rs_pack_ex(grads, s_chunks, "bf16", stream), 2 * E + 2 * W * S),
         "rs_pack_bf16_to_f32": (lambda: plan.rs_pack_ex(grads, s32_chunks, "f32", stream), 2 * E + 4 * W * S),

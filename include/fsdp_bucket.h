@@ -199,8 +199,9 @@ fsdp_status fsdp_rs_reduce(const fsdp_plan* plan, int32_t rank, const uint16_t* 
  *   - the bucket buffers as W separate chunks.  chunks[i] points at rank i's
  *     chunk of S elements, so an exchange can be fused with the copy: pull
  *     the gathered chunks straight from the peers' send chunks, push each
- *     destination's chunk straight into that peer's receive buffer, and pull
- *     the W received chunks from the peers' send buffers.
+ *     destination's chunk straight into that peer's receive buffer, pull
+ *     the W received chunks from the peers' send buffers, or push one
+ *     packed chunk into every peer's gathered buffer.
  * Layouts, zero filling, numerics and error behaviour are those of the
  * calls above; chunks[] is a host array of W <= FSDP_MAX_CHUNKS device
  * pointers, each 16-byte aligned.  Errors: as above, plus FSDP_ERR_TOO_MANY
@@ -212,6 +213,14 @@ fsdp_status fsdp_rs_reduce(const fsdp_plan* plan, int32_t rank, const uint16_t* 
  * fp32 shards).  send_chunk holds S elements of param_dtype. */
 fsdp_status fsdp_ag_pack_ex(const fsdp_plan* plan, int32_t rank, const float* const* shards,
                             fsdp_dtype param_dtype, void* send_chunk, hipStream_t stream);
+
+/* fsdp_ag_pack_ex pushing the packed chunk to W destinations: chunks[i] is
+ * where rank i receives this rank's chunk (slot `rank` of rank i's gathered
+ * buffer), so the one-shot all-gather is fused with the copy-in.  Each of the
+ * W chunks receives the same S elements of param_dtype; the shards are read
+ * once.  The chunks must not overlap each other or the shards. */
+fsdp_status fsdp_ag_pack_push(const fsdp_plan* plan, int32_t rank, const float* const* shards,
+                              fsdp_dtype param_dtype, void* const* chunks, hipStream_t stream);
 
 /* fsdp_ag_unpack from W chunk pointers (rank i's chunk at chunks[i]); params
  * and chunks hold param_dtype elements. */

@@ -40,6 +40,8 @@ SIGNATURES = {
     "fsdp_rs_reduce": (c_status, [c_plan_p, ctypes.c_int32, ctypes.c_void_p, c_ptr_array, ctypes.c_void_p]),
     "fsdp_ag_pack_ex": (c_status, [c_plan_p, ctypes.c_int32, c_ptr_array, ctypes.c_int32, ctypes.c_void_p,
                                    ctypes.c_void_p]),
+    "fsdp_ag_pack_push": (c_status, [c_plan_p, ctypes.c_int32, c_ptr_array, ctypes.c_int32, c_ptr_array,
+                                     ctypes.c_void_p]),
     "fsdp_ag_unpack_ex": (c_status, [c_plan_p, ctypes.c_int32, c_ptr_array, c_ptr_array, ctypes.c_void_p]),
     "fsdp_rs_pack_ex": (c_status, [c_plan_p, ctypes.c_int32, c_ptr_array, ctypes.c_int32, c_ptr_array,
                                    ctypes.c_void_p]),

@@ -189,6 +189,17 @@ class BucketPlan:
         _check(self._lib.fsdp_ag_pack_ex(self._h, int(rank), arr, _dtype_code(param_dtype), dst,
                                          _stream_handle(stream)), "fsdp_ag_pack_ex")
 
+    def ag_pack_push(self, rank: int, shards: Sequence[torch.Tensor], chunks: Sequence[torch.Tensor],
+                     param_dtype: str = "bf16", stream=None) -> None:
+        """fp32 shards -> the packed chunk of ``param_dtype``, written to each of the W
+        ``chunks`` (where every rank receives this rank's chunk)."""
+        self._check_len(shards, "shards")
+        arr = _ptr_array(shards, [self.local_elems(p, rank) for p in range(self.num_params)],
+                         (torch.float32,), "shards")
+        carr = self._chunk_array(chunks, _elem_dtypes(param_dtype))
+        _check(self._lib.fsdp_ag_pack_push(self._h, int(rank), arr, _dtype_code(param_dtype), carr,
+                                           _stream_handle(stream)), "fsdp_ag_pack_push")
+
     def ag_unpack_ex(self, chunks: Sequence[torch.Tensor], params: Sequence[torch.Tensor],
                      param_dtype: str = "bf16", stream=None) -> None:
         """W gathered chunks (rank i's at chunks[i]) -> full parameters of ``param_dtype``."""

@@ -251,12 +251,22 @@ __device__ __forceinline__ void seg_widen(const uint16_t* __restrict__ s, float*
 
 // ------------------------------------------------------------------ ag_pack
 
+// One destination chunk (the rank's send chunk).
+struct OneChunk {
+    char* ptr;
+    __device__ __forceinline__ char* at(int) const { return ptr; }
+};
+
+// Dst is OneChunk, or TableChunks when the packed chunk is pushed to W
+// destinations (the peers' gathered buffers), each receiving the same bytes.
+template <class Dst>
 struct PackArgs {
     const float* src[PMAX];
     int64_t off[PMAX + 1];       // off[P] = S
     int64_t valid[PMAX];         // n_{p,rank} * inner_p
     int32_t tile_start[PMAX];
-    void* dst;                   // bf16 or fp32 chunk of S elements
+    Dst dst;                     // bf16 or fp32 chunks of S elements
+    int32_t ndst;                // destinations (1 for OneChunk)
     int32_t nparams;
     int32_t ntiles;
 };
@@ -267,31 +277,37 @@ __device__ __forceinline__ uint2 cast4(float4 a) {
 }
 
 // Tile lt of parameter p: its part of [off_p, off_{p+1}) of the chunk, the
-// shard's values cast to bf16 (kCast) or copied as fp32, zeros past the shard.
-// Each thread handles 4 elements per sub-step (16 bytes of fp32 in), so every
-// load and store instruction of a wave covers one contiguous run.
-template <bool kCast>
-__device__ __forceinline__ void pack_tile(const PackArgs& a, int p, int lt) {
+// shard's values cast to bf16 (kCast) or copied as fp32, zeros past the shard,
+// written to every destination.  Each thread handles 4 elements per sub-step
+// (16 bytes of fp32 in), so every load and store instruction of a wave covers
+// one contiguous run.
+template <bool kCast, class Dst>
+__device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt) {
     typedef typename std::conditional<kCast, uint16_t, uint32_t>::type Out;
     constexpr int kSub = 2 * kPackSteps;
+    constexpr bool kOne = std::is_same<Dst, OneChunk>::value;
+    const int ndst = kOne ? 1 : a.ndst;
     const int64_t off = a.off[p];
     const int64_t region = a.off[p + 1] - off;
     const int64_t valid = a.valid[p];
     const float* __restrict__ src = a.src[p];
-    Out* __restrict__ dst = static_cast<Out*>(a.dst) + off;
     const int64_t lo = int64_t(lt) * kPackTile;
     const int64_t hi = min(lo + kPackTile, region);
     if (lo >= hi) return;
-    const bool vec = is_aligned16(src) && is_aligned16(dst);
+    // every destination chunk is 16-byte aligned, so one test covers them all
+    const bool vec = is_aligned16(src) && is_aligned16(reinterpret_cast<Out*>(a.dst.at(0)) + off);
     if (vec && hi - lo == kPackTile && lo + kPackTile <= valid) {
         float4 x[kSub];
 #pragma unroll
         for (int u = 0; u < kSub; ++u) x[u] = ldf16(src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4);
+        for (int j = 0; j < ndst; ++j) {
+            Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
 #pragma unroll
-        for (int u = 0; u < kSub; ++u) {
-            const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
-            if (kCast) st8(dst + g, cast4(x[u]));
-            else stf16(reinterpret_cast<float*>(dst + g), x[u]);
+            for (int u = 0; u < kSub; ++u) {
+                const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
+                if (kCast) st8(dst + g, cast4(x[u]));
+                else stf16(reinterpret_cast<float*>(dst + g), x[u]);
+            }
         }
         return;
     }
@@ -300,25 +316,28 @@ __device__ __forceinline__ void pack_tile(const PackArgs& a, int p, int lt) {
         if (g >= hi) break;
         if (vec && g + 4 <= hi && (g + 4 <= valid || g >= valid)) {
             const float4 x = g < valid ? ldf16(src + g) : make_float4(0.f, 0.f, 0.f, 0.f);
-            if (kCast) st8(dst + g, g < valid ? cast4(x) : make_uint2(0, 0));
-            else st16(dst + g, g < valid ? make_uint4(__float_as_uint(x.x), __float_as_uint(x.y),
-                                                      __float_as_uint(x.z), __float_as_uint(x.w))
-                                         : make_uint4(0, 0, 0, 0));
+            for (int j = 0; j < ndst; ++j) {
+                Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
+                if (kCast) st8(dst + g, g < valid ? cast4(x) : make_uint2(0, 0));
+                else st16(dst + g, g < valid ? make_uint4(__float_as_uint(x.x), __float_as_uint(x.y),
+                                                          __float_as_uint(x.z), __float_as_uint(x.w))
+                                             : make_uint4(0, 0, 0, 0));
+            }
             continue;
         }
         for (int e = 0; e < 4; ++e) {
             const int64_t k = g + e;
             if (k >= hi) break;
-            if (kCast) dst[k] = k < valid ? Out(bf16_bits(src[k])) : Out(0);
-            else dst[k] = k < valid ? Out(__float_as_uint(src[k])) : Out(0);
+            const Out v = k < valid ? Out(kCast ? bf16_bits(src[k]) : __float_as_uint(src[k])) : Out(0);
+            for (int j = 0; j < ndst; ++j) (reinterpret_cast<Out*>(a.dst.at(j)) + off)[k] = v;
         }
     }
 }
 
 // Tiles numbered across the bucket; the parameter of a tile comes from the
 // wave-ballot lookup.
-template <bool kCast>
-__global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs a) {
+template <bool kCast, class Dst>
+__global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs<Dst> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
@@ -773,38 +792,49 @@ int64_t tiles(int64_t n, int64_t tile) { return (n + tile - 1) / tile; }
 
 // ---- ag_pack
 
-fsdp_status do_ag_pack(const fsdp_plan* h, int32_t rank, const float* const* shards, fsdp_dtype wire,
-                       void* send_chunk, hipStream_t stream) {
+// `dst` is the send chunk (OneChunk) or the W destination chunks
+// (TableChunks); `outs` holds their byte spans for the overlap check.
+template <class Dst>
+fsdp_status do_ag_pack(const Plan& pl, int32_t rank, const float* const* shards, fsdp_dtype wire, const Dst& dst,
+                       int ndst, const std::vector<Span>& outs, hipStream_t stream) {
+    fsdp_status st;
+    if (rank < 0 || rank >= pl.world) return fail(FSDP_ERR_INVALID, "rank out of range");
+    if (shards == nullptr) return fail(FSDP_ERR_INVALID, "shards is NULL");
+    PackArgs<Dst> a{};
+    std::vector<Span> ins;
+    int64_t nt = 0;   // at most the planner's checked pack tile count
+    for (int p = 0; p < pl.nparams; ++p) {
+        const int64_t v = pl.local_elems(p, rank);
+        if ((st = check_param_ptr(shards[p], v, 4, p, "shards")) != FSDP_OK) return st;
+        a.src[p] = shards[p];
+        a.off[p] = pl.off[p];
+        a.valid[p] = v;
+        a.tile_start[p] = int32_t(nt);
+        nt += tiles(pl.off[p + 1] - pl.off[p], kPackTile);
+        if (v > 0) ins.push_back(span(shards[p], v * 4));
+    }
+    a.off[pl.nparams] = pl.chunk;
+    a.dst = dst;
+    a.ndst = ndst;
+    a.nparams = pl.nparams;
+    if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
+    a.ntiles = int32_t(nt);
+    if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
+    if (wire == FSDP_DTYPE_BF16) return launch(ag_pack_kernel<true, Dst>, a, a.ntiles, kCopyBlock, stream);
+    return launch(ag_pack_kernel<false, Dst>, a, a.ntiles, kCopyBlock, stream);
+}
+
+fsdp_status do_ag_pack_one(const fsdp_plan* h, int32_t rank, const float* const* shards, fsdp_dtype wire,
+                           void* send_chunk, hipStream_t stream) {
     clear_error();
     fsdp_status st = FSDP_OK;
     const Plan* pl = get_plan(h, &st);
     if (!pl) return st;
     if (!known_dtype(wire)) return fail(FSDP_ERR_INVALID, "unknown dtype");
-    if (rank < 0 || rank >= pl->world) return fail(FSDP_ERR_INVALID, "rank out of range");
-    if (shards == nullptr) return fail(FSDP_ERR_INVALID, "shards is NULL");
     if ((st = check_bucket_ptr(send_chunk, pl->chunk, "send_chunk")) != FSDP_OK) return st;
-    PackArgs a{};
-    std::vector<Span> ins;
-    int64_t nt = 0;   // at most the planner's checked pack tile count
-    for (int p = 0; p < pl->nparams; ++p) {
-        const int64_t v = pl->local_elems(p, rank);
-        if ((st = check_param_ptr(shards[p], v, 4, p, "shards")) != FSDP_OK) return st;
-        a.src[p] = shards[p];
-        a.off[p] = pl->off[p];
-        a.valid[p] = v;
-        a.tile_start[p] = int32_t(nt);
-        nt += tiles(pl->off[p + 1] - pl->off[p], kPackTile);
-        if (v > 0) ins.push_back(span(shards[p], v * 4));
-    }
-    a.off[pl->nparams] = pl->chunk;
-    a.dst = send_chunk;
-    a.nparams = pl->nparams;
-    if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
-    a.ntiles = int32_t(nt);
-    if (pl->chunk > 0 && (st = check_overlap({span(send_chunk, pl->chunk * elem_bytes(wire))}, ins)) != FSDP_OK)
-        return st;
-    if (wire == FSDP_DTYPE_BF16) return launch(ag_pack_kernel<true>, a, a.ntiles, kCopyBlock, stream);
-    return launch(ag_pack_kernel<false>, a, a.ntiles, kCopyBlock, stream);
+    std::vector<Span> outs;
+    if (pl->chunk > 0) outs.push_back(span(send_chunk, pl->chunk * elem_bytes(wire)));
+    return do_ag_pack(*pl, rank, shards, wire, OneChunk{static_cast<char*>(send_chunk)}, 1, outs, stream);
 }
 
 // ---- ag_unpack: u = 2-byte units per element
@@ -920,12 +950,27 @@ using namespace fsdp;
 
 extern "C" fsdp_status fsdp_ag_pack(const fsdp_plan* h, int32_t rank, const float* const* shards,
                                     uint16_t* send_chunk, hipStream_t stream) {
-    return do_ag_pack(h, rank, shards, FSDP_DTYPE_BF16, send_chunk, stream);
+    return do_ag_pack_one(h, rank, shards, FSDP_DTYPE_BF16, send_chunk, stream);
 }
 
 extern "C" fsdp_status fsdp_ag_pack_ex(const fsdp_plan* h, int32_t rank, const float* const* shards,
                                        fsdp_dtype param_dtype, void* send_chunk, hipStream_t stream) {
-    return do_ag_pack(h, rank, shards, param_dtype, send_chunk, stream);
+    return do_ag_pack_one(h, rank, shards, param_dtype, send_chunk, stream);
+}
+
+extern "C" fsdp_status fsdp_ag_pack_push(const fsdp_plan* h, int32_t rank, const float* const* shards,
+                                         fsdp_dtype param_dtype, void* const* chunks, hipStream_t stream) {
+    clear_error();
+    fsdp_status st = FSDP_OK;
+    const Plan* pl = get_plan(h, &st);
+    if (!pl) return st;
+    if (!known_dtype(param_dtype)) return fail(FSDP_ERR_INVALID, "unknown dtype");
+    TableChunks dst{};
+    std::vector<Span> outs;
+    if ((st = load_chunk_table(*pl, const_cast<const void* const*>(chunks), elem_bytes(param_dtype), &dst, &outs)) !=
+        FSDP_OK)
+        return st;
+    return do_ag_pack(*pl, rank, shards, param_dtype, dst, pl->world, outs, stream);
 }
 
 extern "C" fsdp_status fsdp_ag_unpack(const fsdp_plan* h, const uint16_t* gathered, uint16_t* const* params,

@@ -262,11 +262,20 @@ def test_extended_calls_reject_bad_arguments():
     assert LIB.fsdp_ag_unpack_ex(h, 0, chunks, ptrs(FAKE + (1 << 20) + 16, FAKE + (1 << 24)), None) == OVERLAP
     # fp32 outputs need 4-byte alignment
     assert LIB.fsdp_ag_unpack_ex(h, 1, chunks, ptrs(FAKE + (1 << 24) + 2, FAKE + (1 << 25)), None) == ALIGN
+    # the push: unknown dtype, NULL table, overlapping destinations, a destination over a shard
+    assert LIB.fsdp_ag_pack_push(h, 0, shards, 5, chunks, None) == INVALID
+    assert LIB.fsdp_ag_pack_push(h, 0, shards, 0, None, None) == INVALID
+    assert LIB.fsdp_ag_pack_push(h, 4, shards, 0, chunks, None) == INVALID
+    assert LIB.fsdp_ag_pack_push(h, 0, shards, 0, ptrs(FAKE, FAKE + 16, FAKE + 4096 * 8, FAKE + 4096 * 9),
+                                 None) == OVERLAP
+    assert LIB.fsdp_ag_pack_push(h, 0, ptrs(FAKE + (1 << 20) + 16, FAKE + 8192), 0, chunks, None) == OVERLAP
+    assert LIB.fsdp_ag_pack_push(h, 0, shards, 1, ptrs(FAKE, FAKE + 8, FAKE + 4096, FAKE + 8192), None) == ALIGN
     LIB.fsdp_plan_free(h)
     # more chunks than the table holds
     st_, h = raw_plan(129, [(300, 2)])
     assert st_ == OK
     many = ptrs(*[FAKE + 4096 * i for i in range(129)])
+    assert LIB.fsdp_ag_pack_push(h, 0, ptrs(FAKE + (1 << 30)), 0, many, None) == TOO_MANY
     assert LIB.fsdp_rs_reduce_ex(h, 0, 0, many, ptrs(FAKE + (1 << 30)), None) == TOO_MANY
     assert LIB.fsdp_ag_unpack_ex(h, 0, many, ptrs(FAKE + (1 << 30)), None) == TOO_MANY
     LIB.fsdp_plan_free(h)
@@ -281,6 +290,7 @@ def test_extended_valid_calls_reach_the_runtime():
     assert LIB.fsdp_ag_unpack_ex(h, 1, chunks, ptrs(FAKE + 65536), None) == HIP
     assert LIB.fsdp_rs_pack_ex(h, 0, ptrs(FAKE + 65536), 1, chunks, None) == HIP
     assert LIB.fsdp_rs_reduce_ex(h, 1, 1, chunks, ptrs(FAKE + 65536), None) == HIP
+    assert LIB.fsdp_ag_pack_push(h, 1, ptrs(FAKE + 65536), 0, chunks, None) == HIP
     LIB.fsdp_plan_free(h)
 
 

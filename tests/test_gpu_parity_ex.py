@@ -144,6 +144,34 @@ def test_ex_small(case, align):
     plan.close()
 
 
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_ag_pack_push(case):
+    """The packed chunk of one rank written to W separate destinations, bf16
+    and fp32: every destination equals the oracle's pack."""
+    W, dims = CASES[case]
+    for align in (8, 1):
+        plan = BucketPlan(W, dims, align)
+        oplan = O.make_plan(W, dims, align)
+        S = oplan.chunk
+        P = len(dims)
+        for r in sorted({0, W - 1}):
+            shards = [random_bits32([case, r, p, 11], O.local_elems(oplan, p, r)).view(np.float32) for p in range(P)]
+            bufs = [Guarded(s_.size, torch.float32, r % 2) for s_ in shards]
+            for b, s_ in zip(bufs, shards):
+                if s_.size:
+                    b.view.copy_(to_dev_f32(s_))
+            for dtype in ("bf16", "f32"):
+                dsts = _chunks(W, S, dtype)
+                step(f"ag_pack_push {dtype} W={W} case={case} rank={r} align={align}")
+                plan.ag_pack_push(r, [b.view for b in bufs], [d.view for d in dsts], dtype)
+                torch.cuda.synchronize()
+                want = _bits(O.ag_pack(oplan, r, shards, dtype))
+                for j, d in enumerate(dsts):
+                    assert d.guards_intact(), j
+                    assert np.array_equal(_bits(_host(d.view, dtype)), want), (dtype, j)
+        plan.close()
+
+
 @pytest.mark.parametrize("cap", [1, 7])
 def test_ex_grid_stride(cap, monkeypatch):
     """The element-type and chunk-table forms with every workgroup looping over
@@ -194,6 +222,17 @@ def test_ex_workload_full(key):
         torch.cuda.synchronize()
         assert out.guards_intact()
         assert np.array_equal(host_u32(out.view), O.ag_pack(oplan, r, shards, "f32").view(np.uint32))
+    # the bf16 pack of rank 1 pushed to all W gathered buffers
+    r = 1
+    shards = [random_bits32([key, r, p, 12], O.local_elems(oplan, p, r)).view(np.float32) for p in range(P)]
+    dsts = [torch.empty(S, dtype=torch.bfloat16, device=DEV) for _ in range(W)]
+    step(f"ag_pack_push bf16 full W={W} rank={r}")
+    plan.ag_pack_push(r, [to_dev_f32(s_) for s_ in shards], dsts)
+    torch.cuda.synchronize()
+    want = O.ag_pack(oplan, r, shards)
+    for j in range(W):
+        assert np.array_equal(host_u16(dsts[j]), want), j
+    del dsts, want
     # bf16 gradients cast to an fp32 wire, pushed into W chunks
     grads = [dev_random_bits16(n * k, 300 + p) for p, (n, k) in enumerate(wl.dims)]
     chunks = [torch.empty(S, dtype=torch.float32, device=DEV) for _ in range(W)]
