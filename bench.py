@@ -40,7 +40,7 @@ KERNELS = ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")
 # device symbols of the kernels each call launches on a Llama block (ag_pack
 # takes the 2-D grid kernel there); rocprofv3 reports them by these names
 KERNEL_SYMBOLS = {
-    "ag_pack": "ag_pack_kernel<true>",
+    "ag_pack": "ag_pack_kernel<true, OneChunk>",
     "ag_unpack": "ag_unpack_kernel<ContigChunks>",
     "rs_pack": "rs_pack_kernel<ContigChunks, false>",
     "rs_reduce": "rs_reduce_kernel<ContigChunks, unsigned short>",
