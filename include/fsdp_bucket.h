@@ -67,7 +67,7 @@ enum {
     FSDP_ERR_INVALID = 1,   /* bad argument value, NULL where data is needed, unknown plan */
     FSDP_ERR_ALIGN = 2,     /* bucket buffer not 16-byte aligned, or element misalignment */
     FSDP_ERR_OVERFLOW = 3,  /* a size does not fit the library's 64-bit / tile limits */
-    FSDP_ERR_TOO_MANY = 4,  /* more than FSDP_MAX_PARAMS parameters in one bucket */
+    FSDP_ERR_TOO_MANY = 4,  /* more than FSDP_MAX_PARAMS parameters, or W > FSDP_MAX_CHUNKS in a chunk table */
     FSDP_ERR_NOMEM = 5,     /* host allocation of a plan failed */
     FSDP_ERR_HIP = 6,       /* the HIP runtime reported an error at launch */
     FSDP_ERR_OVERLAP = 7    /* an output overlaps an input or another output */
