@@ -51,3 +51,24 @@ def test_norms_are_one_and_values_are_scaled_normals():
 def test_random_bits_deterministic():
     assert np.array_equal(random_bits16([1, 2], 1000), random_bits16([1, 2], 1000))
     assert not np.array_equal(random_bits16([1, 2], 1000), random_bits16([1, 3], 1000))
+
+
+def test_workload_sizes_match_the_worked_table():
+    """E, S and W*S of every workload, from the oracle's planner and the
+    library's, against tests/golden/workload_sizes.txt."""
+    import oracle.fsdp_oracle as O
+    rows = [[int(x) for x in r] for r in read_table("workload_sizes.txt")]
+    for key, W, P, E, S, WS in rows:
+        wl = WORKLOADS[key]
+        assert (wl.world_size, wl.num_params, wl.total_elems) == (W, P, E)
+        plan = O.make_plan(W, wl.dims, 8)
+        assert plan.chunk == S and W * S == WS
+        if key <= 4:
+            assert WS == E
+        try:
+            from paper_2411_00284_amd import BucketPlan
+        except ImportError:
+            continue
+        bp = BucketPlan(W, wl.dims, 8)
+        assert bp.chunk_elems == S
+        bp.close()
