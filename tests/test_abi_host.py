@@ -306,3 +306,56 @@ def test_widening_pack_tile_count_overflow():
     assert LIB.fsdp_rs_pack_ex(h, 0, ptrs(FAKE + (1 << 46)), 1, chunks, None) == OVERFLOW
     assert b"tiles" in LIB.fsdp_last_error()
     LIB.fsdp_plan_free(h)
+
+
+def test_last_error_is_per_thread():
+    """Each thread reads the detail of its own last failed call."""
+    import threading
+    results = {}
+
+    def worker(i):
+        h = ctypes.c_void_p()
+        rows = (ctypes.c_int64 * 1)(4)
+        inner = (ctypes.c_int64 * 1)(4)
+        msgs = []
+        for _ in range(200):
+            if i % 2:
+                st_ = LIB.fsdp_bucket_plan(0, 1, rows, inner, 8, ctypes.byref(h))        # bad W
+            else:
+                st_ = LIB.fsdp_bucket_plan(4, 1, rows, inner, 3, ctypes.byref(h))        # bad align
+            msgs.append((st_, LIB.fsdp_last_error()))
+        results[i] = msgs
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(8)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    for i, msgs in results.items():
+        want = b"world_size" if i % 2 else b"power of two"
+        assert all(st_ == INVALID and want in m for st_, m in msgs), i
+
+
+def test_plans_from_many_threads():
+    """Plans created, queried and freed concurrently agree with the oracle."""
+    import threading
+    errors = []
+
+    def worker(i):
+        try:
+            for k in range(50):
+                w = 1 + (i * 7 + k) % 64
+                dims = [(1 + (i + k) % 300, 1 + k % 5), (k % 17, 3)]
+                want = O.make_plan(w, dims, 8)
+                got = BucketPlan(w, dims, 8)
+                assert got.chunk_elems == want.chunk
+                got.close()
+        except Exception as e:   # noqa: BLE001 - reported below
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(8)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
