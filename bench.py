@@ -242,6 +242,7 @@ def main(argv=None):
         "cpu_baseline": cpu,
         "variants": variants,
         "auto_wrap": None if args.no_variants else time_auto_wrap(wl),
+        "copy_cost": None if args.no_variants else fit_copy_cost(wl, stream),
     }
     print(json.dumps(line), flush=True)
     plan.close()
@@ -329,6 +330,70 @@ def time_auto_wrap(wl, layers=80, reps=20):
             buckets = auto_wrap(ag, t, m, 20e-6, 2 / 100e9, 8 << 30, backward, ag, 20e-6, 2 / 100e9)
             times.append(time.perf_counter() - t0)
         res[name] = {"buckets": len(buckets), "us_per_pass": round(float(np.median(times)) * 1e6, 1)}
+    return res
+
+
+def fit_copy_cost(wl, stream, reps=5):
+    """Copy-in + copy-out cost of a bucket as a function of its size, on this
+    GPU: buckets made of subsets of the workload's block (one norm up to the
+    whole block) are timed for the forward pair (ag_pack + ag_unpack) and the
+    backward pair (rs_pack + rs_reduce), with a 1 GiB cache flush before each
+    rep, and T = alpha + beta * bytes is fitted by least squares over the
+    algorithmic bytes of the pair.  This is the measured copy part of the
+    alpha-beta model that auto-wrapping prices buckets with."""
+    import numpy as np
+    import torch
+
+    from paper_2411_00284_amd import BucketPlan
+
+    W = wl.world_size
+    names = list(wl.names)
+    sets = [[len(names) - 1], [1], [1, 2], [0], [0, 1, 2, 3], [4], [4, 5, 6], list(range(len(names)))]
+    dev = torch.device("cuda:0")
+    flush = torch.empty(1 << 28, dtype=torch.int32, device=dev)
+    pts = {"forward": [], "backward": []}
+    for sel in sets:
+        dims = [wl.dims[p] for p in sel]
+        plan = BucketPlan(W, dims)
+        S = plan.chunk_elems
+        V0 = sum(plan.local_elems(p, 0) for p in range(len(dims)))
+        E = sum(n * k for n, k in dims)
+        shards = [torch.zeros(plan.local_elems(p, 0), device=dev) for p in range(len(dims))]
+        gathered = torch.zeros(W * S, dtype=torch.bfloat16, device=dev)
+        params = [torch.empty(n * k, dtype=torch.bfloat16, device=dev) for n, k in dims]
+        outs = [torch.empty(plan.local_elems(p, 0), device=dev) for p in range(len(dims))]
+        pairs = {
+            "forward": (lambda: (plan.ag_pack(0, shards, gathered[:S], stream),
+                                 plan.ag_unpack(gathered, params, stream)), 4 * V0 + 2 * S + 4 * E),
+            "backward": (lambda: (plan.rs_pack(params, gathered, stream),
+                                  plan.rs_reduce(0, gathered, outs, stream)), 2 * E + 2 * W * S + 2 * W * V0 + 4 * V0),
+        }
+        for name, (fn, nbytes) in pairs.items():
+            fn()
+            torch.cuda.synchronize()
+            times = []
+            for k in range(reps):
+                flush.fill_(k)
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                fn()
+                b.record(stream)
+                b.synchronize()
+                times.append(a.elapsed_time(b) * 1e3)
+            pts[name].append((nbytes, float(np.median(times))))
+        plan.close()
+        del shards, gathered, params, outs
+    del flush
+    res = {}
+    for name, xy in pts.items():
+        x = np.array([p[0] for p in xy], dtype=np.float64)
+        y = np.array([p[1] for p in xy], dtype=np.float64)
+        beta, alpha = np.polyfit(x, y, 1)
+        pred = alpha + beta * x
+        r2 = 1.0 - float(np.sum((y - pred) ** 2) / np.sum((y - y.mean()) ** 2))
+        res[name] = {"alpha_us": round(float(alpha), 2), "GBps": round(1e-3 / float(beta), 1),
+                     "r2": round(r2, 5), "points": [[int(a), round(b, 2)] for a, b in xy]}
     return res
 
 
