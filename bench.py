@@ -95,7 +95,7 @@ def main(argv=None):
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: one GPU only (asked for --gpus {args.gpus}); "
               "the path has no collective and runs per rank", file=sys.stderr)
         return 2
 

@@ -82,7 +82,7 @@ def load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             f"{LIB_PATH} is not built: run `python -m paper_2411_00284_amd.build` "
-            "(or __graft_entry__.build()) first; there is no fallback path")
+            "first; there is no fallback path")
     lib = ctypes.CDLL(LIB_PATH)
     for name, (res, args) in SIGNATURES.items():
         fn = getattr(lib, name)
