@@ -142,21 +142,22 @@ def main(argv=None):
 
     stream = torch.cuda.current_stream()
 
-    def run_step(ev=None):
+    def run_step(ev=None, st=None):
+        st = stream if st is None else st
         if ev is not None:
-            ev[0].record(stream)
-        plan.ag_pack(rank, shards, send_chunk, stream)
+            ev[0].record(st)
+        plan.ag_pack(rank, shards, send_chunk, st)
         if ev is not None:
-            ev[1].record(stream)
-        plan.ag_unpack(gathered, params, stream)
+            ev[1].record(st)
+        plan.ag_unpack(gathered, params, st)
         if ev is not None:
-            ev[2].record(stream)
-        plan.rs_pack(grads, send_buf, stream)
+            ev[2].record(st)
+        plan.rs_pack(grads, send_buf, st)
         if ev is not None:
-            ev[3].record(stream)
-        plan.rs_reduce(rank, recv, outs, stream)
+            ev[3].record(st)
+        plan.rs_reduce(rank, recv, outs, st)
         if ev is not None:
-            ev[4].record(stream)
+            ev[4].record(st)
 
     for _ in range(args.warmup):
         run_step()
@@ -243,6 +244,8 @@ def main(argv=None):
         "variants": variants,
         "auto_wrap": None if args.no_variants else time_auto_wrap(wl),
         "copy_cost": None if args.no_variants else fit_copy_cost(wl, stream),
+        "graph": None if args.no_variants else time_graph_step(
+            lambda: run_step(None, torch.cuda.current_stream()), args.steps),
     }
     print(json.dumps(line), flush=True)
     plan.close()
@@ -331,6 +334,33 @@ def time_auto_wrap(wl, layers=80, reps=20):
             times.append(time.perf_counter() - t0)
         res[name] = {"buckets": len(buckets), "us_per_pass": round(float(np.median(times)) * 1e6, 1)}
     return res
+
+
+def time_graph_step(run_step, steps):
+    """The same step captured once in a HIP graph (torch.cuda.CUDAGraph) and
+    replayed ``steps`` times back to back: wall time per step.  The four calls
+    allocate nothing and make no memset, so they can be captured; the replay
+    removes the host launch cost, which matters only for small buckets."""
+    import torch
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run_step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run_step()
+    graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / steps * 1e3
+    del graph
+    return {"ms_per_step": round(ms, 4)}
 
 
 def fit_copy_cost(wl, stream, reps=5):
