@@ -33,15 +33,18 @@ Readings where the paper is silent (each also listed in the design notes):
   a multiple of the alignment ``align`` (elements); each per-rank chunk has
   S elements; pad rows, alignment gaps and the chunk tail hold +0.0;
 * the 16-bit format is bf16 with IEEE-754 round-half-to-even; a NaN maps to
-  a quiet NaN of the same sign (payload not part of the contract);
+  a quiet NaN of the same sign (payload not part of the contract); fp16
+  (IEEE binary16, also round-half-to-even, with subnormals and overflow to
+  infinity) is the other 16-bit float the paper's wording allows, and is
+  supported as a param_dtype / reduce_dtype too;
 * the gathered buffer is rank-major [W][S]; the reduce-scatter send buffer is
   destination-major [W][S];
 * the average: fp32 sum over source ranks 0..W-1 in that order, starting
   from the rank-0 value, then one correctly rounded division by W;
 * all fp32 arithmetic keeps subnormals (numpy does not flush them).
 
-Representation: bf16 data is held as ``uint16`` bit patterns, fp32 data as
-``numpy.float32``.
+Representation: bf16 data is held as ``uint16`` bit patterns, fp16 data as
+``numpy.float16``, fp32 data as ``numpy.float32``.
 """
 
 from __future__ import annotations
@@ -58,6 +61,7 @@ __all__ = [
     "local_elems",
     "bf16_rne",
     "bf16_to_f32",
+    "f16_rne",
     "ag_pack",
     "all_gather",
     "ag_unpack",
@@ -181,6 +185,19 @@ def bf16_to_f32(bits) -> np.ndarray:
     return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
+def f16_rne(x) -> np.ndarray:
+    """fp32 -> IEEE-754 binary16 (fp16) values, round-half-to-even.
+
+    numpy's float32 -> float16 conversion, a library routine: the nearest
+    binary16 value with ties to an even significand, subnormals below 2^-14,
+    +-0 below half the smallest subnormal, and infinity from 65520 (the
+    largest finite value plus half an ulp) up.  A NaN gives a NaN; its payload
+    is not part of the contract.
+    """
+    with np.errstate(over="ignore"):
+        return np.asarray(x, dtype=np.float32).astype(np.float16)
+
+
 # --------------------------------------------------------------------------
 # Forward: all-gather copy-in / exchange / copy-out
 # --------------------------------------------------------------------------
@@ -192,7 +209,8 @@ def ag_pack(plan: Plan, rank: int, shards: Sequence[np.ndarray], param_dtype: st
     n_{p,rank} x inner_p.  Output: the rank's chunk of S elements, with shard p
     cast to ``param_dtype`` at off_p and zeros everywhere else (pad rows, gaps,
     tail).  ``param_dtype`` is "bf16" (mixed precision: bf16 bit patterns as
-    uint16) or "f32" (no mixed precision: the fp32 values themselves).
+    uint16), "f16" (mixed precision with fp16: numpy float16 values) or "f32"
+    (no mixed precision: the fp32 values themselves).
     """
     if not 0 <= rank < plan.world_size:
         raise ValueError("rank out of range")
@@ -204,16 +222,23 @@ def ag_pack(plan: Plan, rank: int, shards: Sequence[np.ndarray], param_dtype: st
         if src.size != v:
             raise ValueError(f"shard {p} has {src.size} elements, expected {v}")
         o = plan.offset[p]
-        send[o:o + v] = bf16_rne(src) if param_dtype == "bf16" else src
+        if param_dtype == "bf16":
+            send[o:o + v] = bf16_rne(src)
+        elif param_dtype == "f16":
+            send[o:o + v] = f16_rne(src)
+        else:
+            send[o:o + v] = src
     return send
 
 
 def _wire_dtype(name: str):
     if name == "bf16":
         return np.uint16
+    if name == "f16":
+        return np.float16
     if name == "f32":
         return np.float32
-    raise ValueError("dtype must be 'bf16' or 'f32'")
+    raise ValueError("dtype must be 'bf16', 'f16' or 'f32'")
 
 
 def all_gather(chunks: Sequence[np.ndarray]) -> np.ndarray:
@@ -259,19 +284,21 @@ def rs_pack(plan: Plan, grads: Sequence[np.ndarray], reduce_dtype: str | None = 
     Each full gradient G_p (rows x inner) is zero-padded along dim 0 to
     W * c_p rows and split into W chunks of c_p rows; chunk j goes to
     destination j's part of the send buffer at j*S + off_p.  Everything the
-    chunks do not cover is zero.  Gradients are bf16 bit patterns (uint16) or
-    fp32.  ``reduce_dtype="f32"`` casts bf16 gradients to fp32 first (an exact
-    widening); by default the buffer keeps the gradients' own type.
+    chunks do not cover is zero.  Gradients are bf16 bit patterns (uint16),
+    fp16 or fp32.  ``reduce_dtype="f32"`` casts 16-bit gradients to fp32 first
+    (an exact widening); by default the buffer keeps the gradients' own type.
     """
     W, S = plan.world_size, plan.chunk
     gs = [np.asarray(g) for g in grads]
     if reduce_dtype == "f32":
         gs = [bf16_to_f32(g) if g.dtype == np.uint16 else g.astype(np.float32) for g in gs]
-    elif reduce_dtype not in (None, "bf16"):
-        raise ValueError("reduce_dtype must be 'bf16' or 'f32'")
+    elif reduce_dtype not in (None, "bf16", "f16"):
+        raise ValueError("reduce_dtype must be 'bf16', 'f16' or 'f32'")
     dtype = gs[0].dtype if gs else np.uint16
     if reduce_dtype == "bf16" and dtype != np.uint16:
         raise ValueError("a bf16 wire needs bf16 gradients")
+    if reduce_dtype == "f16" and dtype != np.float16:
+        raise ValueError("an fp16 wire needs fp16 gradients")
     send = np.zeros(W * S, dtype=dtype)
     for p in range(plan.num_params):
         n, k, c, L, o = (plan.rows[p], plan.inner[p], plan.rows_per_rank[p],
@@ -295,8 +322,8 @@ def rs_reduce(plan: Plan, rank: int, recv: np.ndarray) -> list[np.ndarray]:
     """O6, the rank-local average and read-out (section 3.2.1; section 4 reduce_dtype).
 
     For every element of the rank's Shard(0) slab of parameter p: take the W
-    incoming values x_0..x_{W-1} in fp32 (bf16 bit patterns are widened,
-    exactly; an fp32 buffer is used as it is), start from x_0, add x_1, ...,
+    incoming values x_0..x_{W-1} in fp32 (bf16 bit patterns and fp16 values
+    are widened, exactly; an fp32 buffer is used as it is), start from x_0, add x_1, ...,
     x_{W-1} one at a time in fp32, then divide once by W in fp32.  Output: the
     fp32 gradient shards, n_{p,rank} x inner_p (no padded rows).
     """

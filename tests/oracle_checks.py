@@ -496,3 +496,126 @@ def check_rs_reduce_bruteforce_f32(impl, w, dims, rank, seed, align=8):
             for i in range(1, w):
                 a = round_f32(a + float(recv[i * S + plan.offset[p] + e]))
             assert float(flat[e]) == round_f32(a / w), (p, e)
+
+
+# ---------------------------------------------------------------- fp16 variants
+
+def f16_bits_to_float(b: int) -> float:
+    """Decode a binary16 bit pattern from its fields (no numpy float16)."""
+    sign = -1.0 if b >> 15 else 1.0
+    e = (b >> 10) & 0x1F
+    m = b & 0x3FF
+    if e == 0x1F:
+        return sign * math.inf if m == 0 else math.nan
+    if e == 0:
+        return sign * m * 2.0 ** -24
+    return sign * (1.0 + m / 1024.0) * 2.0 ** (e - 15)
+
+
+def _f16_bits(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float16).view(np.uint16)
+
+
+def check_f16_hex_table(impl):
+    for inp, out, *_ in read_table("f16_rne_cases.txt"):
+        got = int(_f16_bits(impl.f16_rne(f32_from_bits([int(inp, 16)])))[0])
+        assert got == int(out, 16), f"f16({inp}) = {got:#06x}, table says {out}"
+
+
+def check_f16_vs_torch(impl, n=1 << 16):
+    u = random_bits32([7, 21], n)
+    x = f32_from_bits(u)
+    ours = _f16_bits(impl.f16_rne(x))
+    ref = torch.from_numpy(x.copy()).to(torch.float16).view(torch.int16).numpy().view(np.uint16)
+    nan = np.isnan(x)
+    assert np.array_equal(ours[~nan], ref[~nan])
+    o = ours[nan]
+    assert np.all(((o & 0x7C00) == 0x7C00) & ((o & 0x3FF) != 0))
+
+
+def check_f16_nearest_even(impl, n=400):
+    """Brute force from the definition: the nearest of all finite binary16
+    values (decoded from their fields), ties to an even significand, and
+    infinity at or beyond the largest finite value plus half an ulp."""
+    codes = np.arange(0, 0x7C00, dtype=np.int64)                 # finite, non-negative
+    vals = np.array([f16_bits_to_float(int(c)) for c in codes])
+    rng = np.random.default_rng([7, 22])
+    mant = rng.standard_normal(n) * np.exp2(rng.integers(-27, 18, n))
+    x = mant.astype(np.float32)
+    got = _f16_bits(impl.f16_rne(x))
+    limit = 65504.0 + 16.0                                       # half an ulp above the top
+    for k in range(n):
+        xv = float(x[k])
+        a = abs(xv)
+        if a >= limit:
+            want = 0x7C00
+        else:
+            d = np.abs(vals - a)
+            best = np.flatnonzero(d == d.min())
+            want = int(codes[best[0]]) if best.size == 1 else int(codes[best[np.argmax(codes[best] % 2 == 0)]])
+        if xv < 0 or (xv == 0 and math.copysign(1.0, xv) < 0):
+            want |= 0x8000
+        assert int(got[k]) == want, f"x={xv!r} got {int(got[k]):#06x} want {want:#06x}"
+
+
+def check_f16_param_roundtrip(impl, w, dims, seed, align=8):
+    """param_dtype fp16: the gathered, unpacked parameters equal torch's fp16
+    cast of the full fp32 parameters; padding is +0."""
+    plan = impl.make_plan(w, dims, align)
+    xs = [np.asarray(np.random.default_rng([seed, p, 23]).standard_normal((n, k))
+                     * np.exp2(np.random.default_rng([seed, p, 24]).integers(-26, 18, (n, k))), np.float32)
+          for p, (n, k) in enumerate(dims)]
+    chunks = []
+    for r in range(w):
+        local = []
+        for p, (n, k) in enumerate(dims):
+            parts = torch.chunk(torch.from_numpy(xs[p]), w, dim=0) if n else ()
+            local.append(parts[r].numpy() if r < len(parts) else np.zeros((0, k), np.float32))
+        send = impl.ag_pack(plan, r, local, param_dtype="f16")
+        assert send.dtype == np.float16 and send.shape == (plan.chunk,)
+        mask = np.ones(plan.chunk, bool)
+        for p in range(len(dims)):
+            v = impl.local_rows(plan, p, r) * dims[p][1]
+            mask[plan.offset[p]:plan.offset[p] + v] = False
+        assert np.all(_f16_bits(send)[mask] == 0)
+        chunks.append(send)
+    out = impl.ag_unpack(plan, np.concatenate(chunks))
+    for p in range(len(dims)):
+        want = torch.from_numpy(xs[p]).to(torch.float16).view(torch.int16).numpy().view(np.uint16)
+        assert out[p].dtype == np.float16
+        assert np.array_equal(_f16_bits(out[p]), want), p
+
+
+def check_f16_wire(impl, w, dims, rank, seed, align=8):
+    """fp16 gradients: an fp16 wire and an fp32 wire give the same bits
+    (widening is exact), and each output equals the binary64-rounded-per-step
+    brute force over the decoded fp16 inputs."""
+    plan = impl.make_plan(w, dims, align)
+    S = plan.chunk
+    rng = np.random.default_rng([seed, 25])
+    grads = []
+    for i in range(w):
+        gi = []
+        for n, k in dims:
+            bits = (rng.integers(0, 0x7C00, (n, k)) | (rng.integers(0, 2, (n, k)) << 15)).astype(np.uint16)
+            gi.append(bits.view(np.float16))
+        grads.append(gi)
+    s16 = [impl.rs_pack(plan, g, reduce_dtype="f16") for g in grads]
+    s32 = [impl.rs_pack(plan, g, reduce_dtype="f32") for g in grads]
+    for a, b in zip(s16, s32):
+        assert a.dtype == np.float16 and b.dtype == np.float32
+        dec = np.array([f16_bits_to_float(int(v)) for v in _f16_bits(a)[:4096]])
+        assert np.array_equal(dec, b[:4096].astype(np.float64))
+    recv16 = _exchange(s16, rank, S)
+    r16 = impl.rs_reduce(plan, rank, recv16)
+    r32 = impl.rs_reduce(plan, rank, _exchange(s32, rank, S))
+    bits = _f16_bits(recv16)
+    for p, (n, k) in enumerate(dims):
+        assert np.array_equal(r16[p].view(np.uint32), r32[p].view(np.uint32)), p
+        nr = impl.local_rows(plan, p, rank)
+        flat = r16[p].reshape(-1)
+        for e in range(nr * k):
+            a_ = f16_bits_to_float(int(bits[plan.offset[p] + e]))
+            for i in range(1, w):
+                a_ = round_f32(a_ + f16_bits_to_float(int(bits[i * S + plan.offset[p] + e])))
+            assert float(flat[e]) == round_f32(a_ / w), (p, e)

@@ -28,7 +28,7 @@ SMALL_CASES = [
 
 def oracle_impl():
     return SimpleNamespace(
-        make_plan=O.make_plan, local_rows=O.local_rows, bf16_rne=O.bf16_rne,
+        make_plan=O.make_plan, local_rows=O.local_rows, bf16_rne=O.bf16_rne, f16_rne=O.f16_rne,
         ag_pack=O.ag_pack, ag_unpack=O.ag_unpack, rs_pack=O.rs_pack, rs_reduce=O.rs_reduce)
 
 
@@ -289,3 +289,65 @@ def test_fp32_pins_catch_a_rounding_pack():
     impl.ag_pack = rounding_pack
     with pytest.raises(AssertionError):
         C.check_f32_param_roundtrip(impl, 3, [(7, 3), (2, 5)], seed=1)
+
+
+# ----------------------------------------------------------------- fp16 wires
+
+def run_f16_checks(impl):
+    C.check_f16_hex_table(impl)
+    C.check_f16_vs_torch(impl)
+    C.check_f16_nearest_even(impl)
+    for w, dims in SMALL_CASES[:4]:
+        C.check_f16_param_roundtrip(impl, w, dims, seed=w)
+        C.check_f16_wire(impl, w, dims, w - 1, seed=w)
+
+
+def test_fp16_variants():
+    run_f16_checks(oracle_impl())
+
+
+def _f16_truncate(x):
+    """Round toward zero (what a packed round-toward-zero conversion does)."""
+    x = np.asarray(x, np.float32)
+    r = x.astype(np.float16)
+    back = r.astype(np.float32)
+    step = np.nextafter(r, np.float16(0)).astype(np.float16)
+    return np.where(np.isfinite(x) & (np.abs(back) > np.abs(x)), step, np.where(np.isinf(r) & np.isfinite(x),
+                    np.copysign(np.float16(65504), x).astype(np.float16), r)).astype(np.float16)
+
+
+def _f16_flush_subnormals(x):
+    r = np.asarray(x, np.float32).astype(np.float16)
+    return np.where(np.abs(r.astype(np.float32)) < 2.0 ** -14, np.copysign(np.float16(0), r), r).astype(np.float16)
+
+
+def _f16_via_bf16(x):
+    """A cast that rounds to bf16 first (double rounding)."""
+    return O.bf16_to_f32(O.bf16_rne(x)).astype(np.float16)
+
+
+F16_MUTANTS = {
+    "fp16 round toward zero": _f16_truncate,
+    "fp16 subnormals flushed": _f16_flush_subnormals,
+    "fp16 double rounding through bf16": _f16_via_bf16,
+}
+
+
+@pytest.mark.parametrize("name", sorted(F16_MUTANTS))
+def test_fp16_pins_catch_mutant(name):
+    impl = oracle_impl()
+    cast = F16_MUTANTS[name]
+    impl.f16_rne = cast
+
+    def pack(plan, rank, shards, param_dtype="bf16"):
+        if param_dtype != "f16":
+            return O.ag_pack(plan, rank, shards, param_dtype)
+        send = np.zeros(plan.chunk, np.float16)
+        for p in range(plan.num_params):
+            v = O.local_elems(plan, p, rank)
+            send[plan.offset[p]:plan.offset[p] + v] = cast(np.asarray(shards[p]).reshape(-1))
+        return send
+    impl.ag_pack = pack
+    with pytest.raises(AssertionError):
+        with np.errstate(all="ignore"):
+            run_f16_checks(impl)
