@@ -37,12 +37,12 @@ if ROOT not in sys.path:
 METRIC = "effective HBM GB/s (and % of peak) for bucket pack/unpack/reduce"
 PEAK_GBPS = 8000.0                       # MI355X HBM3E
 KERNELS = ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")
-# device symbols of the kernels each call launches on a Llama block (ag_pack
-# takes the 2-D grid kernel there); rocprofv3 reports them by these names
+# device symbols of the kernels each call launches (bf16 wire, one contiguous
+# buffer); rocprofv3 reports them by these names
 KERNEL_SYMBOLS = {
-    "ag_pack": "ag_pack_kernel<true, OneChunk>",
+    "ag_pack": "ag_pack_kernel<1, OneChunk>",
     "ag_unpack": "ag_unpack_kernel<ContigChunks>",
-    "rs_pack": "rs_pack_kernel<ContigChunks, false>",
+    "rs_pack": "rs_pack_kernel<ContigChunks, 0>",
     "rs_reduce": "rs_reduce_kernel<ContigChunks, unsigned short>",
 }
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_00284_amd", "csrc", "bucket_kernels.hip")
@@ -90,6 +90,11 @@ def main(argv=None):
     ap.add_argument("--variant-reps", type=int, default=10)
     ap.add_argument("--event-every", type=int, default=5,
                     help="record the per-kernel HIP events on every N-th timed step (N=1: every step)")
+    ap.add_argument("--copy-cost", action="store_true",
+                    help="also fit the alpha + beta*bytes copy cost over sub-buckets of the block "
+                         "(launches the path kernels at other sizes, so it is off in profiled runs)")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step replayed from a HIP graph")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the steps, run a plain 1 GiB device copy (for counter scaling)")
     args = ap.parse_args(argv)
@@ -243,8 +248,8 @@ def main(argv=None):
         "cpu_baseline": cpu,
         "variants": variants,
         "auto_wrap": None if args.no_variants else time_auto_wrap(wl),
-        "copy_cost": None if args.no_variants else fit_copy_cost(wl, stream),
-        "graph": None if args.no_variants else time_graph_step(
+        "copy_cost": fit_copy_cost(wl, stream) if args.copy_cost else None,
+        "graph": None if not args.graph else time_graph_step(
             lambda: run_step(None, torch.cuda.current_stream()), args.steps),
     }
     print(json.dumps(line), flush=True)
@@ -254,10 +259,10 @@ def main(argv=None):
 
 def time_variants(plan, wl, rank, shards, gathered, params, grads, send_buf, recv, outs, stream, reps):
     """Average launch time of the element-type and chunk-table forms, on the
-    same bucket: fp32 param_dtype pack, the pack pushed to W chunks,
+    same bucket: fp32 and fp16 param_dtype packs, the pack pushed to W chunks,
     W-chunk-table unpack / pack / reduce
     (tables pointing into the same buffers), bf16 gradients cast to an fp32
-    wire, and the fp32 reduce."""
+    wire, and the fp32 and fp16 reduces."""
     import numpy as np
     import torch
 
@@ -274,14 +279,19 @@ def time_variants(plan, wl, rank, shards, gathered, params, grads, send_buf, rec
     r_chunks = [recv[i * S:(i + 1) * S] for i in range(W)]
     s32_chunks = [send32[i * S:(i + 1) * S] for i in range(W)]
     r32_chunks = [recv32[i * S:(i + 1) * S] for i in range(W)]
+    send_chunk16 = torch.empty(S, dtype=torch.float16, device=dev)
+    recv16 = recv.view(torch.float16)                   # the same bytes read as fp16 (timing only)
+    r16_chunks = [recv16[i * S:(i + 1) * S] for i in range(W)]
     cases = {
         "ag_pack_f32": (lambda: plan.ag_pack_ex(rank, shards, send_chunk32, "f32", stream), 4 * V0 + 4 * S),
+        "ag_pack_f16": (lambda: plan.ag_pack_ex(rank, shards, send_chunk16, "f16", stream), 4 * V0 + 2 * S),
         "ag_pack_push": (lambda: plan.ag_pack_push(rank, shards, s_chunks, "bf16", stream), 4 * V0 + 2 * W * S),
         "ag_unpack_chunks": (lambda: plan.ag_unpack_ex(g_chunks, params, "bf16", stream), 4 * E),
         "rs_pack_chunks": (lambda: plan.rs_pack_ex(grads, s_chunks, "bf16", stream), 2 * E + 2 * W * S),
         "rs_pack_bf16_to_f32": (lambda: plan.rs_pack_ex(grads, s32_chunks, "f32", stream), 2 * E + 4 * W * S),
         "rs_reduce_chunks": (lambda: plan.rs_reduce_ex(rank, r_chunks, outs, "bf16", stream), 2 * W * V0 + 4 * V0),
         "rs_reduce_f32": (lambda: plan.rs_reduce_ex(rank, r32_chunks, outs, "f32", stream), 4 * W * V0 + 4 * V0),
+        "rs_reduce_f16": (lambda: plan.rs_reduce_ex(rank, r16_chunks, outs, "f16", stream), 2 * W * V0 + 4 * V0),
     }
     flush = torch.empty(1 << 28, dtype=torch.int32, device=dev)   # 1 GiB: evicts L2 and the 256 MB MALL
     res = {}
@@ -302,7 +312,7 @@ def time_variants(plan, wl, rank, shards, gathered, params, grads, send_buf, rec
         gbps = nbytes / (avg_ms * 1e-3) / 1e9
         res[name] = {"avg_us": round(avg_ms * 1e3, 2), "bytes": nbytes, "GBps": round(gbps, 1),
                      "frac": round(gbps / PEAK_GBPS, 4)}
-    del send_chunk32, send32, recv32, flush
+    del send_chunk32, send32, recv32, send_chunk16, flush
     return res
 
 

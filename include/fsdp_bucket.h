@@ -82,9 +82,11 @@ enum {
 #define FSDP_MAX_CHUNKS 128
 
 /* Element types of the *_ex entry points (section 4: param_dtype and
- * reduce_dtype). */
+ * reduce_dtype).  BF16 and F16 (IEEE binary16) are the two 16-bit floats;
+ * fp32 -> 16-bit casts round to nearest even (NaN -> a NaN), 16-bit -> fp32
+ * is exact. */
 typedef int32_t fsdp_dtype;
-enum { FSDP_DTYPE_BF16 = 0, FSDP_DTYPE_F32 = 1 };
+enum { FSDP_DTYPE_BF16 = 0, FSDP_DTYPE_F32 = 1, FSDP_DTYPE_F16 = 2 };
 
 typedef struct fsdp_plan fsdp_plan;
 
@@ -209,8 +211,8 @@ fsdp_status fsdp_rs_reduce(const fsdp_plan* plan, int32_t rank, const uint16_t* 
  * ---------------------------------------------------------------------------
  */
 
-/* fsdp_ag_pack with param_dtype BF16 (the cast) or F32 (a bit copy of the
- * fp32 shards).  send_chunk holds S elements of param_dtype. */
+/* fsdp_ag_pack with param_dtype BF16 or F16 (the cast) or F32 (a bit copy
+ * of the fp32 shards).  send_chunk holds S elements of param_dtype. */
 fsdp_status fsdp_ag_pack_ex(const fsdp_plan* plan, int32_t rank, const float* const* shards,
                             fsdp_dtype param_dtype, void* send_chunk, hipStream_t stream);
 
@@ -228,8 +230,9 @@ fsdp_status fsdp_ag_unpack_ex(const fsdp_plan* plan, fsdp_dtype param_dtype, con
                               void* const* params, hipStream_t stream);
 
 /* fsdp_rs_pack into W chunk pointers (destination j's chunk at chunks[j]).
- * grad_dtype BF16 with reduce_dtype BF16 or F32 (exact widening), or both
- * F32; F32 gradients on a BF16 wire are refused (FSDP_ERR_INVALID). */
+ * reduce_dtype is grad_dtype (a copy) or F32 (16-bit gradients widened
+ * exactly); any other pair, such as F32 gradients on a 16-bit wire, would
+ * be a rounding step and is refused (FSDP_ERR_INVALID). */
 fsdp_status fsdp_rs_pack_ex(const fsdp_plan* plan, fsdp_dtype grad_dtype, const void* const* grads,
                             fsdp_dtype reduce_dtype, void* const* chunks, hipStream_t stream);
 

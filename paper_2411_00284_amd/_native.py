@@ -58,6 +58,7 @@ MAX_PARAMS = 64
 MAX_CHUNKS = 128
 DTYPE_BF16 = 0
 DTYPE_F32 = 1
+DTYPE_F16 = 2
 
 _lib = None
 

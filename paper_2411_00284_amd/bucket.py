@@ -17,25 +17,27 @@ import torch
 from . import _native
 
 BF16_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
+F16_DTYPES = (torch.float16,)
 F32_DTYPES = (torch.float32, torch.int32)
-_DTYPE_CODES = {"bf16": 0, "f32": 1}
+_DTYPE_CODES = {"bf16": 0, "f32": 1, "f16": 2}
+_DTYPES = {"bf16": BF16_DTYPES, "f16": F16_DTYPES, "f32": F32_DTYPES}
 
 
 def _dtype_code(name: str) -> int:
     if name not in _DTYPE_CODES:
-        raise ValueError("dtype must be 'bf16' or 'f32'")
+        raise ValueError("dtype must be 'bf16', 'f16' or 'f32'")
     return _DTYPE_CODES[name]
 
 
 def _elem_dtypes(name: str):
-    return BF16_DTYPES if name == "bf16" else F32_DTYPES
+    _dtype_code(name)
+    return _DTYPES[name]
 
 
 def _dtype_name(t: torch.Tensor) -> str:
-    if t.dtype in BF16_DTYPES:
-        return "bf16"
-    if t.dtype in F32_DTYPES:
-        return "f32"
+    for name, dtypes in _DTYPES.items():
+        if t.dtype in dtypes:
+            return name
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
@@ -181,7 +183,7 @@ class BucketPlan:
     # ---- element-type and chunk-table forms
     def ag_pack_ex(self, rank: int, shards: Sequence[torch.Tensor], send_chunk: torch.Tensor,
                    param_dtype: str = "bf16", stream=None) -> None:
-        """fp32 shards -> a chunk of ``param_dtype`` ("bf16" cast or "f32" copy)."""
+        """fp32 shards -> a chunk of ``param_dtype`` ("bf16" or "f16" cast, or "f32" copy)."""
         self._check_len(shards, "shards")
         arr = _ptr_array(shards, [self.local_elems(p, rank) for p in range(self.num_params)],
                          (torch.float32,), "shards")
@@ -212,7 +214,8 @@ class BucketPlan:
 
     def rs_pack_ex(self, grads: Sequence[torch.Tensor], chunks: Sequence[torch.Tensor],
                    reduce_dtype: str = "bf16", stream=None) -> None:
-        """Full gradients (bf16 or fp32) -> W destination chunks of ``reduce_dtype``."""
+        """Full gradients (bf16, f16 or fp32) -> W destination chunks of ``reduce_dtype``
+        (the gradients' type, or "f32")."""
         self._check_len(grads, "grads")
         names = {_dtype_name(g) for g in grads if g is not None}
         if len(names) > 1:

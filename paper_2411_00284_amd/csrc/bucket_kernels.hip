@@ -74,6 +74,30 @@ __device__ __forceinline__ uint32_t bf16x2_bits(float lo, float hi) {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// IEEE binary16: the conversion instruction rounds to nearest even under the
+// default mode, keeps subnormals and overflows to infinity; the way back is
+// exact.
+__device__ __forceinline__ uint32_t f16_bits(float f) {
+    return __builtin_bit_cast(uint16_t, static_cast<_Float16>(f));
+}
+__device__ __forceinline__ float f16_lo(uint32_t w) {
+    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xffffu)));
+}
+__device__ __forceinline__ float f16_hi(uint32_t w) {
+    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16)));
+}
+
+// Element formats a kernel reads or writes on a bucket wire.
+constexpr int kF32 = 0;    // fp32, copied bit for bit
+constexpr int kBF16 = 1;   // bf16
+constexpr int kF16 = 2;    // IEEE binary16
+
+// The exact fp32 value of the low / high 16-bit element of a word.
+template <int kFrom>
+__device__ __forceinline__ float widen_lo(uint32_t w) { return kFrom == kF16 ? f16_lo(w) : bf16_lo(w); }
+template <int kFrom>
+__device__ __forceinline__ float widen_hi(uint32_t w) { return kFrom == kF16 ? f16_hi(w) : bf16_hi(w); }
+
 // Parameter owning tile t: the last p with tile_start[p] <= t.  Every lane of
 // the wave holds tile_start[lane] (INT_MAX past the last parameter).
 __device__ __forceinline__ int param_of_tile(int my_start, int t) {
@@ -209,10 +233,11 @@ __device__ __forceinline__ void seg_copy(const uint16_t* __restrict__ s, uint16_
     }
 }
 
-// As seg_copy, but bf16 elements in and their exact fp32 values out.  Each
-// thread handles 4 elements per sub-step (8 bytes in, 16 bytes out), so that
-// every load and store instruction of a wave covers one contiguous run.
-template <int kSteps>
+// As seg_copy, but 16-bit elements (bf16 or fp16, kFrom) in and their exact
+// fp32 values out.  Each thread handles 4 elements per sub-step (8 bytes in,
+// 16 bytes out), so that every load and store instruction of a wave covers
+// one contiguous run.
+template <int kSteps, int kFrom>
 __device__ __forceinline__ void seg_widen(const uint16_t* __restrict__ s, float* __restrict__ d, int64_t lo,
                                           int64_t hi, int64_t v, bool vec) {
     constexpr int kSub = kSteps;
@@ -225,7 +250,7 @@ __device__ __forceinline__ void seg_widen(const uint16_t* __restrict__ s, float*
 #pragma unroll
             for (int u = 0; u < kSub; ++u)
                 stf16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4,
-                      make_float4(bf16_lo(x[u].x), bf16_hi(x[u].x), bf16_lo(x[u].y), bf16_hi(x[u].y)));
+                      make_float4(widen_lo<kFrom>(x[u].x), widen_hi<kFrom>(x[u].x), widen_lo<kFrom>(x[u].y), widen_hi<kFrom>(x[u].y)));
         } else {
 #pragma unroll
             for (int u = 0; u < kSub; ++u)
@@ -238,13 +263,14 @@ __device__ __forceinline__ void seg_widen(const uint16_t* __restrict__ s, float*
         if (g >= hi) break;
         if (vec && g + 4 <= hi && (g + 4 <= v || g >= v)) {
             const uint2 x = g < v ? ld8(s + g) : make_uint2(0, 0);
-            stf16(d + g, make_float4(bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)));
+            stf16(d + g, make_float4(widen_lo<kFrom>(x.x), widen_hi<kFrom>(x.x),
+                                      widen_lo<kFrom>(x.y), widen_hi<kFrom>(x.y)));
             continue;
         }
         for (int e = 0; e < 4; ++e) {
             const int64_t k = g + e;
             if (k >= hi) break;
-            d[k] = k < v ? bf16_lo(s[k]) : 0.f;
+            d[k] = k < v ? widen_lo<kFrom>(s[k]) : 0.f;
         }
     }
 }
@@ -271,18 +297,22 @@ struct PackArgs {
     int32_t ntiles;
 };
 
-// Four fp32 values -> four bf16 bit patterns (8 bytes).
+// Four fp32 values -> four 16-bit patterns (8 bytes) of format kOut.
+template <int kOut>
+__device__ __forceinline__ uint32_t cast1(float f) { return kOut == kF16 ? f16_bits(f) : bf16_bits(f); }
+template <int kOut>
 __device__ __forceinline__ uint2 cast4(float4 a) {
-    return make_uint2(bf16x2_bits(a.x, a.y), bf16x2_bits(a.z, a.w));
+    return make_uint2(cast1<kOut>(a.x) | (cast1<kOut>(a.y) << 16), cast1<kOut>(a.z) | (cast1<kOut>(a.w) << 16));
 }
 
 // Tile lt of parameter p: its part of [off_p, off_{p+1}) of the chunk, the
-// shard's values cast to bf16 (kCast) or copied as fp32, zeros past the shard,
+// shard's values cast to bf16 or fp16 or copied as fp32 (kOut), zeros past the shard,
 // written to every destination.  Each thread handles 4 elements per sub-step
 // (16 bytes of fp32 in), so every load and store instruction of a wave covers
 // one contiguous run.
-template <bool kCast, class Dst>
+template <int kOut, class Dst>
 __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt) {
+    constexpr bool kCast = kOut != kF32;
     typedef typename std::conditional<kCast, uint16_t, uint32_t>::type Out;
     constexpr int kSub = 2 * kPackSteps;
     constexpr bool kOne = std::is_same<Dst, OneChunk>::value;
@@ -305,7 +335,7 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
 #pragma unroll
             for (int u = 0; u < kSub; ++u) {
                 const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
-                if (kCast) st8(dst + g, cast4(x[u]));
+                if (kCast) st8(dst + g, cast4<kOut>(x[u]));
                 else stf16(reinterpret_cast<float*>(dst + g), x[u]);
             }
         }
@@ -318,7 +348,7 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
             const float4 x = g < valid ? ldf16(src + g) : make_float4(0.f, 0.f, 0.f, 0.f);
             for (int j = 0; j < ndst; ++j) {
                 Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
-                if (kCast) st8(dst + g, g < valid ? cast4(x) : make_uint2(0, 0));
+                if (kCast) st8(dst + g, g < valid ? cast4<kOut>(x) : make_uint2(0, 0));
                 else st16(dst + g, g < valid ? make_uint4(__float_as_uint(x.x), __float_as_uint(x.y),
                                                           __float_as_uint(x.z), __float_as_uint(x.w))
                                              : make_uint4(0, 0, 0, 0));
@@ -328,7 +358,7 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
         for (int e = 0; e < 4; ++e) {
             const int64_t k = g + e;
             if (k >= hi) break;
-            const Out v = k < valid ? Out(kCast ? bf16_bits(src[k]) : __float_as_uint(src[k])) : Out(0);
+            const Out v = k < valid ? Out(kCast ? cast1<kOut>(src[k]) : __float_as_uint(src[k])) : Out(0);
             for (int j = 0; j < ndst; ++j) (reinterpret_cast<Out*>(a.dst.at(j)) + off)[k] = v;
         }
     }
@@ -336,13 +366,13 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
 
 // Tiles numbered across the bucket; the parameter of a tile comes from the
 // wave-ballot lookup.
-template <bool kCast, class Dst>
+template <int kOut, class Dst>
 __global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs<Dst> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
         const int p = param_of_tile(my_start, t);
-        pack_tile<kCast>(a, p, t - a.tile_start[p]);
+        pack_tile<kOut>(a, p, t - a.tile_start[p]);
     }
 }
 
@@ -386,8 +416,9 @@ __global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs<
 
 // ------------------------------------------------------------------ rs_pack
 
-// Sizes in units of the source gradient: 2-byte units for a plain copy, bf16
-// elements when kWiden casts them to an fp32 wire.
+// Sizes in units of the source gradient: 2-byte units for a plain copy, 16-bit
+// elements when kWiden (kBF16 or kF16; kF32 = no widening) casts them to an
+// fp32 wire.
 template <class Chunks>
 struct RsPackArgs {
     const uint16_t* src[PMAX];   // full gradients
@@ -401,7 +432,7 @@ struct RsPackArgs {
     int32_t ntiles;
 };
 
-template <class Chunks, bool kWiden>
+template <class Chunks, int kWiden>
 __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Chunks> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
@@ -415,13 +446,13 @@ __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Ch
         const int64_t L = a.seg[p];
         const int64_t rest = a.elems[p] - int64_t(j) * L;
         const int64_t v = rest < L ? (rest > 0 ? rest : 0) : L;
-        constexpr int64_t kTile = kWiden ? kWidenTile : kCopyTile;
+        constexpr int64_t kTile = kWiden != kF32 ? kWidenTile : kCopyTile;
         const int64_t lo = st * kTile;
         const int64_t hi = min(lo + kTile, region);
         const uint16_t* s = a.src[p] + int64_t(j) * L;
-        if (kWiden) {
+        if constexpr (kWiden != kF32) {
             float* d = reinterpret_cast<float*>(a.dst.at(j)) + a.off[p];
-            seg_widen<kCopySteps>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
+            seg_widen<kCopySteps, kWiden>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
         } else {
             uint16_t* d = reinterpret_cast<uint16_t*>(a.dst.at(j)) + a.off[p];
             seg_copy<kCopySteps>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
@@ -470,6 +501,19 @@ template <> struct Raw8<uint16_t> {
     __device__ __forceinline__ void load(const uint16_t* row, uint32_t t) { x = ld16(row + t * 8); }
     __device__ __forceinline__ void init(float (&acc)[8]) const { init8(acc, x); }
     __device__ __forceinline__ void add(float (&acc)[8]) const { add8(acc, x); }
+};
+template <> struct Raw8<_Float16> {
+    uint4 x;
+    __device__ __forceinline__ static uint32_t pos(uint32_t t, int e) { return t * 8 + e; }
+    __device__ __forceinline__ void load(const _Float16* row, uint32_t t) { x = ld16(row + t * 8); }
+    __device__ __forceinline__ void init(float (&acc)[8]) const {
+        acc[0] = f16_lo(x.x); acc[1] = f16_hi(x.x); acc[2] = f16_lo(x.y); acc[3] = f16_hi(x.y);
+        acc[4] = f16_lo(x.z); acc[5] = f16_hi(x.z); acc[6] = f16_lo(x.w); acc[7] = f16_hi(x.w);
+    }
+    __device__ __forceinline__ void add(float (&acc)[8]) const {
+        acc[0] += f16_lo(x.x); acc[1] += f16_hi(x.x); acc[2] += f16_lo(x.y); acc[3] += f16_hi(x.y);
+        acc[4] += f16_lo(x.z); acc[5] += f16_hi(x.z); acc[6] += f16_lo(x.w); acc[7] += f16_hi(x.w);
+    }
 };
 template <> struct Raw8<float> {
     float4 a, b;
@@ -564,7 +608,7 @@ __device__ __forceinline__ void reduce_tile_vec(const Src& src, int64_t off, flo
                 for (int u = 0; u < kReduceSteps; ++u) x[b][u].add(acc[u]);
             }
     }
-    if constexpr (std::is_same<T, uint16_t>::value) {
+    if constexpr (sizeof(T) == 2) {
         // Thread t holds outputs [8t, 8t + 8) of each row: staged through LDS
         // so that every store instruction of a wave covers one contiguous run.
         __shared__ float4 stage[kReduceSteps * kReduceBlock * 2];
@@ -587,6 +631,7 @@ __device__ __forceinline__ void reduce_tile_vec(const Src& src, int64_t off, flo
 }
 
 __device__ __forceinline__ float widen(uint16_t x) { return bf16_lo(x); }
+__device__ __forceinline__ float widen(_Float16 x) { return static_cast<float>(x); }
 __device__ __forceinline__ float widen(float x) { return x; }
 
 // One thread's group of 8 outputs of one row whose group lies wholly inside
@@ -748,7 +793,7 @@ const Plan* get_plan(const fsdp_plan* h, fsdp_status* st) {
     return pl;
 }
 
-bool known_dtype(fsdp_dtype t) { return t == FSDP_DTYPE_BF16 || t == FSDP_DTYPE_F32; }
+bool known_dtype(fsdp_dtype t) { return t == FSDP_DTYPE_BF16 || t == FSDP_DTYPE_F32 || t == FSDP_DTYPE_F16; }
 int elem_bytes(fsdp_dtype t) { return t == FSDP_DTYPE_F32 ? 4 : 2; }
 
 // A host array of W chunk pointers, each 16-byte aligned and non-NULL when
@@ -820,8 +865,9 @@ fsdp_status do_ag_pack(const Plan& pl, int32_t rank, const float* const* shards,
     if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
     a.ntiles = int32_t(nt);
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    if (wire == FSDP_DTYPE_BF16) return launch(ag_pack_kernel<true, Dst>, a, a.ntiles, kCopyBlock, stream);
-    return launch(ag_pack_kernel<false, Dst>, a, a.ntiles, kCopyBlock, stream);
+    if (wire == FSDP_DTYPE_BF16) return launch(ag_pack_kernel<kBF16, Dst>, a, a.ntiles, kCopyBlock, stream);
+    if (wire == FSDP_DTYPE_F16) return launch(ag_pack_kernel<kF16, Dst>, a, a.ntiles, kCopyBlock, stream);
+    return launch(ag_pack_kernel<kF32, Dst>, a, a.ntiles, kCopyBlock, stream);
 }
 
 fsdp_status do_ag_pack_one(const fsdp_plan* h, int32_t rank, const float* const* shards, fsdp_dtype wire,
@@ -869,14 +915,15 @@ fsdp_status do_ag_unpack(const Plan& pl, const Chunks& src, const std::vector<Sp
     return launch(ag_unpack_kernel<Chunks>, a, a.ntiles, kCopyBlock, stream);
 }
 
-// ---- rs_pack: gradient elements of `gsize` bytes; kWiden casts bf16 to fp32
+// ---- rs_pack: gradient elements of `gsize` bytes; kWiden (kBF16 / kF16) casts
+// 16-bit gradients to fp32, kF32 copies
 
-template <class Chunks, bool kWiden>
+template <class Chunks, int kWiden>
 fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, const Chunks& dst,
                        const std::vector<Span>& outs, hipStream_t stream) {
     fsdp_status st;
     if (grads == nullptr) return fail(FSDP_ERR_INVALID, "grads is NULL");
-    const int u = kWiden ? 1 : gsize / 2;             // kernel units per element
+    const int u = kWiden != kF32 ? 1 : gsize / 2;     // kernel units per element
     RsPackArgs<Chunks> a{};
     std::vector<Span> ins;
     int64_t nt = 0;
@@ -887,7 +934,7 @@ fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, cons
         a.off[p] = pl.off[p] * u;
         a.seg[p] = pl.seg[p] * u;
         a.elems[p] = e * u;
-        const int64_t tps = tiles((pl.off[p + 1] - pl.off[p]) * u, kWiden ? kWidenTile : kCopyTile);
+        const int64_t tps = tiles((pl.off[p + 1] - pl.off[p]) * u, kWiden != kF32 ? kWidenTile : kCopyTile);
         if (tps > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
         a.tiles_per_seg[p] = int32_t(tps);
         a.tile_start[p] = int32_t(nt);
@@ -1012,7 +1059,7 @@ extern "C" fsdp_status fsdp_rs_pack(const fsdp_plan* h, const uint16_t* const* g
     std::vector<Span> outs;
     if (total > 0) outs.push_back(span(send_buf, total * 2));
     const ContigChunks dst{reinterpret_cast<char*>(send_buf), pl->chunk * 2};
-    return do_rs_pack<ContigChunks, false>(*pl, reinterpret_cast<const void* const*>(grads), 2, dst, outs, stream);
+    return do_rs_pack<ContigChunks, kF32>(*pl, reinterpret_cast<const void* const*>(grads), 2, dst, outs, stream);
 }
 
 extern "C" fsdp_status fsdp_rs_pack_ex(const fsdp_plan* h, fsdp_dtype grad_dtype, const void* const* grads,
@@ -1022,14 +1069,18 @@ extern "C" fsdp_status fsdp_rs_pack_ex(const fsdp_plan* h, fsdp_dtype grad_dtype
     const Plan* pl = get_plan(h, &st);
     if (!pl) return st;
     if (!known_dtype(grad_dtype) || !known_dtype(reduce_dtype)) return fail(FSDP_ERR_INVALID, "unknown dtype");
-    if (grad_dtype == FSDP_DTYPE_F32 && reduce_dtype == FSDP_DTYPE_BF16)
-        return fail(FSDP_ERR_INVALID, "fp32 gradients on a bf16 wire are not supported");
+    // the wire keeps the gradients' type or widens 16-bit gradients to fp32;
+    // any other pair would be a rounding step the method does not describe
+    if (reduce_dtype != grad_dtype && reduce_dtype != FSDP_DTYPE_F32)
+        return fail(FSDP_ERR_INVALID, "the wire must have the gradients' type or be fp32");
     TableChunks dst{};
     std::vector<Span> outs;
     if ((st = load_chunk_table(*pl, chunks, elem_bytes(reduce_dtype), &dst, &outs)) != FSDP_OK) return st;
     if (grad_dtype == FSDP_DTYPE_BF16 && reduce_dtype == FSDP_DTYPE_F32)
-        return do_rs_pack<TableChunks, true>(*pl, grads, 2, dst, outs, stream);
-    return do_rs_pack<TableChunks, false>(*pl, grads, elem_bytes(grad_dtype), dst, outs, stream);
+        return do_rs_pack<TableChunks, kBF16>(*pl, grads, 2, dst, outs, stream);
+    if (grad_dtype == FSDP_DTYPE_F16 && reduce_dtype == FSDP_DTYPE_F32)
+        return do_rs_pack<TableChunks, kF16>(*pl, grads, 2, dst, outs, stream);
+    return do_rs_pack<TableChunks, kF32>(*pl, grads, elem_bytes(grad_dtype), dst, outs, stream);
 }
 
 extern "C" fsdp_status fsdp_rs_reduce(const fsdp_plan* h, int32_t rank, const uint16_t* recv,
@@ -1059,5 +1110,7 @@ extern "C" fsdp_status fsdp_rs_reduce_ex(const fsdp_plan* h, int32_t rank, fsdp_
     std::vector<Span> ins;
     if ((st = load_chunk_table(*pl, chunks, elem_bytes(reduce_dtype), &src, &ins)) != FSDP_OK) return st;
     if (reduce_dtype == FSDP_DTYPE_F32) return do_rs_reduce<TableChunks, float>(*pl, rank, src, ins, grad_shards, stream);
+    if (reduce_dtype == FSDP_DTYPE_F16)
+        return do_rs_reduce<TableChunks, _Float16>(*pl, rank, src, ins, grad_shards, stream);
     return do_rs_reduce<TableChunks, uint16_t>(*pl, rank, src, ins, grad_shards, stream);
 }

@@ -246,8 +246,11 @@ def test_extended_calls_reject_bad_arguments():
     assert LIB.fsdp_ag_unpack_ex(h, -1, chunks, outs, None) == INVALID
     assert LIB.fsdp_rs_pack_ex(h, 0, shards, 2, chunks, None) == INVALID
     assert LIB.fsdp_rs_reduce_ex(h, 0, 3, chunks, outs, None) == INVALID
-    # fp32 gradients on a bf16 wire
+    # a wire of another 16-bit type, or fp32 gradients on a 16-bit wire
     assert LIB.fsdp_rs_pack_ex(h, 1, shards, 0, chunks, None) == INVALID
+    assert LIB.fsdp_rs_pack_ex(h, 1, shards, 2, chunks, None) == INVALID
+    assert LIB.fsdp_rs_pack_ex(h, 0, shards, 2, chunks, None) == INVALID
+    assert LIB.fsdp_rs_pack_ex(h, 2, shards, 0, chunks, None) == INVALID
     # NULL chunk table, NULL or misaligned chunk
     assert LIB.fsdp_ag_unpack_ex(h, 0, None, outs, None) == INVALID
     assert LIB.fsdp_rs_reduce_ex(h, 0, 0, ptrs(FAKE, FAKE + 64, None, FAKE + 192), outs, None) == INVALID
@@ -291,6 +294,12 @@ def test_extended_valid_calls_reach_the_runtime():
     assert LIB.fsdp_rs_pack_ex(h, 0, ptrs(FAKE + 65536), 1, chunks, None) == HIP
     assert LIB.fsdp_rs_reduce_ex(h, 1, 1, chunks, ptrs(FAKE + 65536), None) == HIP
     assert LIB.fsdp_ag_pack_push(h, 1, ptrs(FAKE + 65536), 0, chunks, None) == HIP
+    # fp16: the pack, the copy and widening packs, the reduce
+    assert LIB.fsdp_ag_pack_ex(h, 0, ptrs(FAKE + 65536), 2, FAKE, None) == HIP
+    assert LIB.fsdp_ag_unpack_ex(h, 2, chunks, ptrs(FAKE + 65536), None) == HIP
+    assert LIB.fsdp_rs_pack_ex(h, 2, ptrs(FAKE + 65536), 2, chunks, None) == HIP
+    assert LIB.fsdp_rs_pack_ex(h, 2, ptrs(FAKE + 65536), 1, chunks, None) == HIP
+    assert LIB.fsdp_rs_reduce_ex(h, 1, 2, chunks, ptrs(FAKE + 65536), None) == HIP
     LIB.fsdp_plan_free(h)
 
 

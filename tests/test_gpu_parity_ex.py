@@ -38,20 +38,40 @@ CASES = [
     (128, [(300, 5), (129, 8), (2, 1)]),            # the chunk-table limit
 ]
 
-TORCH = {"bf16": torch.bfloat16, "f32": torch.float32}
+TORCH = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}
 
 
 def _host(t, dtype):
-    return host_u16(t) if dtype == "bf16" else host_u32(t).view(np.float32)
+    if dtype == "bf16":
+        return host_u16(t)
+    if dtype == "f16":
+        return host_u16(t).view(np.float16)
+    return host_u32(t).view(np.float32)
 
 
 def _to_dev(a, dtype):
-    return to_dev_u16(a) if dtype == "bf16" else to_dev_f32(a)
+    if dtype == "bf16":
+        return to_dev_u16(a)
+    if dtype == "f16":
+        return to_dev_u16(np.asarray(a, np.float16).view(np.uint16)).view(torch.float16)
+    return to_dev_f32(a)
 
 
 def _bits(a):
     a = np.asarray(a)
-    return a.view(np.uint16) if a.dtype == np.uint16 else a.view(np.uint32)
+    return a.view(np.uint16) if a.dtype.itemsize == 2 else a.view(np.uint32)
+
+
+def _same(got, want):
+    """Bit for bit, except that where the oracle holds a float NaN only the
+    class is compared (a NaN's payload after an fp16 conversion is left open)."""
+    got, want = np.asarray(got), np.asarray(want)
+    if want.dtype in (np.float16, np.float32):
+        nan = np.isnan(want)
+        if nan.any():
+            g = got.view(want.dtype)
+            return bool(np.array_equal(np.isnan(g), nan)) and bool(np.array_equal(_bits(g)[~nan], _bits(want)[~nan]))
+    return bool(np.array_equal(_bits(got), _bits(want)))
 
 
 def _chunks(W, S, dtype, host=None):
@@ -85,16 +105,22 @@ def test_ex_small(case, align):
             for b, s in zip(bufs, shards):
                 if s.size:
                     b.view.copy_(to_dev_f32(s))
-            for dtype in ("f32", "bf16"):
+            for dtype in ("f32", "bf16", "f16"):
                 out = Guarded(S, TORCH[dtype])
                 step(f"ag_pack_ex {dtype} W={W} case={case} rank={r} align={align} shift={shift}")
                 plan.ag_pack_ex(r, [b.view for b in bufs], out.view, dtype)
                 torch.cuda.synchronize()
                 assert out.guards_intact()
-                assert np.array_equal(_bits(_host(out.view, dtype)), _bits(O.ag_pack(oplan, r, shards, dtype)))
+                want = O.ag_pack(oplan, r, shards, dtype)
+                assert _same(_host(out.view, dtype), want if dtype != "bf16" else _bits(want))
         # ---- ag_unpack_ex from W separate chunks
-        for dtype in ("bf16", "f32"):
-            g = random_bits16([case, 2], W * S) if dtype == "bf16" else random_bits32([case, 3], W * S).view(np.float32)
+        for dtype in ("bf16", "f32", "f16"):
+            if dtype == "f32":
+                g = random_bits32([case, 3], W * S).view(np.float32)
+            else:
+                g = random_bits16([case, 2], W * S)
+                if dtype == "f16":
+                    g = g.view(np.float16)
             chunks = _chunks(W, S, dtype, g)
             outs = [Guarded(n * k, TORCH[dtype], shift) for n, k in dims]
             step(f"ag_unpack_ex {dtype} W={W} case={case} align={align} shift={shift}")
@@ -105,9 +131,11 @@ def test_ex_small(case, align):
                 assert o.guards_intact(), p
                 assert np.array_equal(_bits(_host(o.view, dtype)), _bits(want[p].reshape(-1))), (dtype, p)
         # ---- rs_pack_ex into W separate chunks: bf16->bf16, bf16->f32, f32->f32
-        for gdt, wire in (("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32")):
+        for gdt, wire in (("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32"), ("f16", "f16"), ("f16", "f32")):
             if gdt == "bf16":
                 grads = [random_bits16([case, 4, p], n * k) for p, (n, k) in enumerate(dims)]
+            elif gdt == "f16":
+                grads = [random_bits16([case, 8, p], n * k).view(np.float16) for p, (n, k) in enumerate(dims)]
             else:
                 grads = [random_bits32([case, 5, p], n * k).view(np.float32) for p, (n, k) in enumerate(dims)]
             gbufs = [Guarded(gg.size, TORCH[gdt], shift) for gg in grads]
@@ -122,13 +150,17 @@ def test_ex_small(case, align):
                              None if gdt == wire else wire)
             for j, c in enumerate(chunks):
                 assert c.guards_intact(), j
-                assert np.array_equal(_bits(_host(c.view, wire)), _bits(want[j * S:(j + 1) * S])), (gdt, wire, j)
+                assert _same(_host(c.view, wire), want[j * S:(j + 1) * S]), (gdt, wire, j)
         # ---- rs_reduce_ex from W separate chunks, bf16 and f32
-        for dtype in ("bf16", "f32"):
+        for dtype in ("bf16", "f32", "f16"):
             if dtype == "bf16":
                 rng = np.random.default_rng([case, 6])
                 recv = ((rng.standard_normal(W * S) * np.exp2(rng.integers(-20, 21, W * S)))
                         .astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+            elif dtype == "f16":
+                rng = np.random.default_rng([case, 9])
+                recv = (rng.integers(0, 0x7C00, W * S) | (rng.integers(0, 2, W * S) << 15)).astype(np.uint16)
+                recv = recv.view(np.float16)
             else:
                 recv = _wide_f32([case, 7], W * S)
             chunks = _chunks(W, S, dtype, recv)
@@ -160,15 +192,15 @@ def test_ag_pack_push(case):
             for b, s_ in zip(bufs, shards):
                 if s_.size:
                     b.view.copy_(to_dev_f32(s_))
-            for dtype in ("bf16", "f32"):
+            for dtype in ("bf16", "f32", "f16"):
                 dsts = _chunks(W, S, dtype)
                 step(f"ag_pack_push {dtype} W={W} case={case} rank={r} align={align}")
                 plan.ag_pack_push(r, [b.view for b in bufs], [d.view for d in dsts], dtype)
                 torch.cuda.synchronize()
-                want = _bits(O.ag_pack(oplan, r, shards, dtype))
+                want = O.ag_pack(oplan, r, shards, dtype)
                 for j, d in enumerate(dsts):
                     assert d.guards_intact(), j
-                    assert np.array_equal(_bits(_host(d.view, dtype)), want), (dtype, j)
+                    assert _same(_host(d.view, dtype), want), (dtype, j)
         plan.close()
 
 
@@ -222,6 +254,15 @@ def test_ex_workload_full(key):
         torch.cuda.synchronize()
         assert out.guards_intact()
         assert np.array_equal(host_u32(out.view), O.ag_pack(oplan, r, shards, "f32").view(np.uint32))
+    # the fp16 pack of rank W-1
+    r = W - 1
+    shards = [random_bits32([key, r, p, 13], O.local_elems(oplan, p, r)).view(np.float32) for p in range(P)]
+    out = Guarded(S, torch.float16)
+    step(f"ag_pack_ex f16 full W={W} rank={r}")
+    plan.ag_pack_ex(r, [to_dev_f32(s_) for s_ in shards], out.view, "f16")
+    torch.cuda.synchronize()
+    assert out.guards_intact()
+    assert _same(_host(out.view, "f16"), O.ag_pack(oplan, r, shards, "f16"))
     # the bf16 pack of rank 1 pushed to all W gathered buffers
     r = 1
     shards = [random_bits32([key, r, p, 12], O.local_elems(oplan, p, r)).view(np.float32) for p in range(P)]

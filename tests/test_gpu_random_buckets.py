@@ -120,6 +120,31 @@ def test_random_bucket(i):
     for p, o in enumerate(outs):
         assert o.guards_intact(), p
         assert np.array_equal(host_u32(o.view), wantr[p].reshape(-1).view(np.uint32)), p
+    # fp16: the pack of rank r, and the reduce of finite fp16 chunks
+    out16 = Guarded(S, torch.float16)
+    step(f"random bucket {i}: ag_pack_ex f16")
+    plan.ag_pack_ex(r, [b.view for b in bufs], out16.view, "f16")
+    torch.cuda.synchronize()
+    assert out16.guards_intact()
+    got16 = host_u16(out16.view).view(np.float16)
+    want16 = O.ag_pack(oplan, r, shards, "f16")
+    nan16 = np.isnan(want16)
+    assert np.array_equal(np.isnan(got16), nan16)
+    assert np.array_equal(got16.view(np.uint16)[~nan16], want16.view(np.uint16)[~nan16])
+    rng16 = np.random.default_rng([6000, i])
+    recv16 = (rng16.integers(0, 0x7C00, W * S) | (rng16.integers(0, 2, W * S) << 15)).astype(np.uint16)
+    chunks16 = [Guarded(S, torch.float16) for _ in range(W)]
+    for j, c in enumerate(chunks16):
+        if S:
+            c.view.copy_(to_dev_u16(recv16[j * S:(j + 1) * S]).view(torch.float16))
+    outs = [Guarded(O.local_elems(oplan, p, r), torch.float32, shift) for p in range(P)]
+    step(f"random bucket {i}: rs_reduce_ex f16 from {W} chunks")
+    plan.rs_reduce_ex(r, [c.view for c in chunks16], [o.view for o in outs], "f16")
+    torch.cuda.synchronize()
+    wantr = O.rs_reduce(oplan, r, recv16.view(np.float16))
+    for p, o in enumerate(outs):
+        assert o.guards_intact(), p
+        assert np.array_equal(host_u32(o.view), wantr[p].reshape(-1).view(np.uint32)), p
     src_chunks = [Guarded(S, torch.bfloat16) for _ in range(W)]
     g = random_bits16([4000, i], W * S)
     for j, c in enumerate(src_chunks):
