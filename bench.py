@@ -1,9 +1,9 @@
 """Benchmark: one rank's bucketed FSDP copy path on one MI355X.
 
 A step is one pass of the whole hot path over one bucket (one transformer
-block) at rank 0:
+block) at one rank (rank 0 unless --rank says otherwise):
 
-    ag_pack (fp32 shards -> bf16 chunk, written into rank 0's slot of the
+    ag_pack (fp32 shards -> bf16 chunk, written into the rank's slot of the
     gathered buffer), ag_unpack (gathered W*S -> full bf16 params),
     rs_pack (full bf16 grads -> W*S send buffer), rs_reduce (W*S received
     chunks -> fp32 grad shards).
@@ -15,9 +15,11 @@ metric is effective HBM bandwidth: the algorithmic bytes of the step (what
 the method must read and write, padding writes included) divided by the
 step time.  Per-kernel launch durations come from HIP events recorded on the
 stream the kernels run on; the dominant kernel's figure is the roofline
-entry.  The CPU oracle is timed on a bounded sample of the same workload.
+entry.  A plain device-to-device copy of the unpack's bytes is timed beside
+them as the achievable reference.  The CPU oracle is timed on a bounded
+sample of the same workload.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 3]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 3] [--rank 0]
 """
 
 from __future__ import annotations
@@ -84,6 +86,7 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3, help="1 toy, 2 8B, 3 70B (default), 4 405B, 5 uneven")
+    ap.add_argument("--rank", type=int, default=0, help="the rank whose share is timed (0 <= rank < W)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip timing the fp32-wire and chunk-table forms after the steps")
@@ -111,7 +114,10 @@ def main(argv=None):
     from synth import workload
 
     wl = workload(args.workload)
-    W, rank = wl.world_size, 0
+    W, rank = wl.world_size, args.rank
+    if not 0 <= rank < W:
+        print(f"bench.py: --rank {rank} is outside 0..{W - 1} for {wl.name}", file=sys.stderr)
+        return 2
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     plan = BucketPlan(W, wl.dims)
@@ -137,7 +143,7 @@ def main(argv=None):
         v = plan.local_elems(p, rank)
         shards.append(torch.ones(v, device=dev) if wl.is_norm[p] else normal(v, 0.02, torch.float32))
     gathered = normal(W * S, 0.02, torch.bfloat16)          # the other ranks' chunks
-    send_chunk = gathered[rank * S:(rank + 1) * S]           # rank 0 packs into its own slot
+    send_chunk = gathered[rank * S:(rank + 1) * S]           # the rank packs into its own slot
     params = [torch.empty(n * k, dtype=torch.bfloat16, device=dev) for n, k in wl.dims]
     grads = [normal(n * k, 1e-3, torch.bfloat16) for n, k in wl.dims]
     send_buf = torch.empty(W * S, dtype=torch.bfloat16, device=dev)
@@ -192,8 +198,12 @@ def main(argv=None):
     for name in KERNELS:
         avg_ms = float(np.mean(per_kernel_ms[name]))
         gbps = abytes[name] / (avg_ms * 1e-3) / 1e9
-        kernels[name] = {"avg_us": round(avg_ms * 1e3, 2), "min_us": round(float(np.min(per_kernel_ms[name])) * 1e3, 2),
+        kernels[name] = {"avg_us": round(avg_ms * 1e3, 2),
+                         "median_us": round(float(np.median(per_kernel_ms[name])) * 1e3, 2),
+                         "min_us": round(float(np.min(per_kernel_ms[name])) * 1e3, 2),
                          "bytes": abytes[name], "GBps": round(gbps, 1), "frac": round(gbps / PEAK_GBPS, 4)}
+
+    copy_ref = None if args.no_variants else time_d2d_copy(gathered, send_buf, stream, args.variant_reps)
 
     variants = None if args.no_variants else time_variants(
         plan, wl, rank, shards, gathered, params, grads, send_buf, recv, outs, stream, args.variant_reps)
@@ -222,7 +232,7 @@ def main(argv=None):
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl)
+        cpu = cpu_baseline(wl, rank)
 
     ms_per_step = elapsed / args.steps * 1e3
     line = {
@@ -245,6 +255,7 @@ def main(argv=None):
         "kernels": kernels,
         "kernel_event_steps": len(per_kernel_ms[KERNELS[0]]),
         "roofline": roofline,
+        "d2d_copy": copy_ref,
         "cpu_baseline": cpu,
         "variants": variants,
         "auto_wrap": None if args.no_variants else time_auto_wrap(wl),
@@ -255,6 +266,35 @@ def main(argv=None):
     print(json.dumps(line), flush=True)
     plan.close()
     return 0
+
+
+def time_d2d_copy(src, dst, stream, reps):
+    """A plain device-to-device copy of ``src`` into ``dst`` (torch ``copy_``
+    of two contiguous same-type tensors, which is the runtime's
+    hipMemcpyAsync), timed with HIP events on ``stream``: the achievable
+    reference for the copy kernels, at the unpack's bytes."""
+    import numpy as np
+    import torch
+
+    nbytes = 2 * src.numel() * src.element_size()
+    with torch.cuda.stream(stream):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        with torch.cuda.stream(stream):
+            dst.copy_(src)
+        b.record(stream)
+        b.synchronize()
+        times.append(a.elapsed_time(b))
+    avg_ms = float(np.mean(times))
+    gbps = nbytes / (avg_ms * 1e-3) / 1e9
+    return {"kind": "hipMemcpyAsync device to device (torch copy_)", "bytes": nbytes,
+            "avg_us": round(avg_ms * 1e3, 2), "median_us": round(float(np.median(times)) * 1e3, 2),
+            "GBps": round(gbps, 1), "frac": round(gbps / PEAK_GBPS, 4)}
 
 
 def time_variants(plan, wl, rank, shards, gathered, params, grads, send_buf, recv, outs, stream, reps):
@@ -437,8 +477,8 @@ def fit_copy_cost(wl, stream, reps=5):
     return res
 
 
-def cpu_baseline(wl, min_seconds=10.0, max_passes=50):
-    """The oracle, as it stands, timed on the host: all four steps at rank 0
+def cpu_baseline(wl, rank=0, min_seconds=10.0, max_passes=50):
+    """The oracle, as it stands, timed on the host: all four steps at ``rank``
     over the whole bucket, repeated until about ``min_seconds`` of CPU work
     has been measured (the oracle is single-threaded numpy)."""
     import numpy as np
@@ -451,8 +491,8 @@ def cpu_baseline(wl, min_seconds=10.0, max_passes=50):
     plan = O.make_plan(W, dims, 8)
     S = plan.chunk
     E = sum(n * k for n, k in dims)
-    V0 = sum(O.local_elems(plan, p, 0) for p in range(len(dims)))
-    shards = [random_bits32([1, p], O.local_elems(plan, p, 0)).view(np.float32) for p in range(len(dims))]
+    V0 = sum(O.local_elems(plan, p, rank) for p in range(len(dims)))
+    shards = [random_bits32([1, p], O.local_elems(plan, p, rank)).view(np.float32) for p in range(len(dims))]
     shards = [np.where(np.isfinite(s), s, np.float32(0)) for s in shards]
     gathered = random_bits16([2], W * S)
     grads = [random_bits16([3, p], n * k).reshape(n, k) for p, (n, k) in enumerate(dims)]
@@ -460,10 +500,10 @@ def cpu_baseline(wl, min_seconds=10.0, max_passes=50):
     t = {k: 0.0 for k in ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")}
     passes = 0
     while passes < max_passes and (passes == 0 or sum(t.values()) < min_seconds):
-        t0 = time.perf_counter(); O.ag_pack(plan, 0, shards); t["ag_pack"] += time.perf_counter() - t0
+        t0 = time.perf_counter(); O.ag_pack(plan, rank, shards); t["ag_pack"] += time.perf_counter() - t0
         t0 = time.perf_counter(); O.ag_unpack(plan, gathered); t["ag_unpack"] += time.perf_counter() - t0
         t0 = time.perf_counter(); O.rs_pack(plan, grads); t["rs_pack"] += time.perf_counter() - t0
-        t0 = time.perf_counter(); O.rs_reduce(plan, 0, recv); t["rs_reduce"] += time.perf_counter() - t0
+        t0 = time.perf_counter(); O.rs_reduce(plan, rank, recv); t["rs_reduce"] += time.perf_counter() - t0
         passes += 1
     b = algorithmic_bytes(W, S, E, V0)
     total_s = sum(t.values())
@@ -473,7 +513,7 @@ def cpu_baseline(wl, min_seconds=10.0, max_passes=50):
         "cores": 1,
         "kind": "oracle",
         "sample": (f"{wl.name}: the whole bucket ({len(dims)} params, W={W}, {sum(b.values())} algorithmic "
-                   f"bytes per pass), all four steps at rank 0, {passes} passes, numpy single thread; "
+                   f"bytes per pass), all four steps at rank {rank}, {passes} passes, numpy single thread; "
                    f"host has {len(os.sched_getaffinity(0))} cores"),
         "seconds": round(total_s, 3),
         "per_pass_s": {k: round(v / passes, 4) for k, v in t.items()},

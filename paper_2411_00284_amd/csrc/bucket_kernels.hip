@@ -149,7 +149,7 @@ __device__ __forceinline__ void st8(void* p, uint2 v) {
     *q = w;
 #endif
 }
-__device__ __forceinline__ float4 ldf16(const float* p) {
+__device__ __forceinline__ float4 ld16f(const float* p) {
     const f32x4* q = reinterpret_cast<const f32x4*>(p);
 #if FSDP_NT_LOAD
     const f32x4 v = __builtin_nontemporal_load(q);
@@ -158,7 +158,7 @@ __device__ __forceinline__ float4 ldf16(const float* p) {
 #endif
     return make_float4(v.x, v.y, v.z, v.w);
 }
-__device__ __forceinline__ void stf16(float* p, float4 v) {
+__device__ __forceinline__ void st16f(float* p, float4 v) {
     f32x4* q = reinterpret_cast<f32x4*>(p);
     const f32x4 w = {v.x, v.y, v.z, v.w};
 #if FSDP_NT_STORE
@@ -249,12 +249,12 @@ __device__ __forceinline__ void seg_widen(const uint16_t* __restrict__ s, float*
             for (int u = 0; u < kSub; ++u) x[u] = ld8(s + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4);
 #pragma unroll
             for (int u = 0; u < kSub; ++u)
-                stf16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4,
+                st16f(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4,
                       make_float4(widen_lo<kFrom>(x[u].x), widen_hi<kFrom>(x[u].x), widen_lo<kFrom>(x[u].y), widen_hi<kFrom>(x[u].y)));
         } else {
 #pragma unroll
             for (int u = 0; u < kSub; ++u)
-                stf16(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4, make_float4(0.f, 0.f, 0.f, 0.f));
+                st16f(d + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4, make_float4(0.f, 0.f, 0.f, 0.f));
         }
         return;
     }
@@ -263,7 +263,7 @@ __device__ __forceinline__ void seg_widen(const uint16_t* __restrict__ s, float*
         if (g >= hi) break;
         if (vec && g + 4 <= hi && (g + 4 <= v || g >= v)) {
             const uint2 x = g < v ? ld8(s + g) : make_uint2(0, 0);
-            stf16(d + g, make_float4(widen_lo<kFrom>(x.x), widen_hi<kFrom>(x.x),
+            st16f(d + g, make_float4(widen_lo<kFrom>(x.x), widen_hi<kFrom>(x.x),
                                       widen_lo<kFrom>(x.y), widen_hi<kFrom>(x.y)));
             continue;
         }
@@ -297,7 +297,8 @@ struct PackArgs {
     int32_t ntiles;
 };
 
-// Four fp32 values -> four 16-bit patterns (8 bytes) of format kOut.
+// One fp32 value -> its 16-bit pattern in format kOut (bf16 or fp16); four
+// values -> four patterns packed in 8 bytes.
 template <int kOut>
 __device__ __forceinline__ uint32_t cast1(float f) { return kOut == kF16 ? f16_bits(f) : bf16_bits(f); }
 template <int kOut>
@@ -329,14 +330,14 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
     if (vec && hi - lo == kPackTile && lo + kPackTile <= valid) {
         float4 x[kSub];
 #pragma unroll
-        for (int u = 0; u < kSub; ++u) x[u] = ldf16(src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4);
+        for (int u = 0; u < kSub; ++u) x[u] = ld16f(src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4);
         for (int j = 0; j < ndst; ++j) {
             Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
 #pragma unroll
             for (int u = 0; u < kSub; ++u) {
                 const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
                 if (kCast) st8(dst + g, cast4<kOut>(x[u]));
-                else stf16(reinterpret_cast<float*>(dst + g), x[u]);
+                else st16f(reinterpret_cast<float*>(dst + g), x[u]);
             }
         }
         return;
@@ -345,7 +346,7 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
         const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
         if (g >= hi) break;
         if (vec && g + 4 <= hi && (g + 4 <= valid || g >= valid)) {
-            const float4 x = g < valid ? ldf16(src + g) : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 x = g < valid ? ld16f(src + g) : make_float4(0.f, 0.f, 0.f, 0.f);
             for (int j = 0; j < ndst; ++j) {
                 Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
                 if (kCast) st8(dst + g, g < valid ? cast4<kOut>(x) : make_uint2(0, 0));
@@ -521,8 +522,8 @@ template <> struct Raw8<float> {
         return e < 4 ? t * 4 + e : uint32_t(kReduceBlock) * 4 + t * 4 + (e - 4);
     }
     __device__ __forceinline__ void load(const float* row, uint32_t t) {
-        a = ldf16(row + t * 4);
-        b = ldf16(row + uint32_t(kReduceBlock) * 4 + t * 4);
+        a = ld16f(row + t * 4);
+        b = ld16f(row + uint32_t(kReduceBlock) * 4 + t * 4);
     }
     __device__ __forceinline__ void init(float (&acc)[8]) const {
         acc[0] = a.x; acc[1] = a.y; acc[2] = a.z; acc[3] = a.w;
@@ -539,8 +540,8 @@ template <typename T>
 __device__ __forceinline__ void store_avg8(float* row, uint32_t t, const float (&acc)[8], float wf) {
     const float4 lo = make_float4(acc[0] / wf, acc[1] / wf, acc[2] / wf, acc[3] / wf);
     const float4 hi = make_float4(acc[4] / wf, acc[5] / wf, acc[6] / wf, acc[7] / wf);
-    stf16(row + Raw8<T>::pos(t, 0), lo);
-    stf16(row + Raw8<T>::pos(t, 4), hi);
+    st16f(row + Raw8<T>::pos(t, 0), lo);
+    st16f(row + Raw8<T>::pos(t, 4), hi);
 }
 
 // Typed pointer to the tile of source i: through the chunk table, or as a
@@ -622,7 +623,7 @@ __device__ __forceinline__ void reduce_tile_vec(const Src& src, int64_t off, flo
         for (int u = 0; u < kReduceSteps; ++u)
 #pragma unroll
             for (int h = 0; h < 2; ++h)
-                stf16(dtile + u * kRow + (h * kReduceBlock + t) * 4, stage[u * kReduceBlock * 2 + h * kReduceBlock + t]);
+                st16f(dtile + u * kRow + (h * kReduceBlock + t) * 4, stage[u * kReduceBlock * 2 + h * kReduceBlock + t]);
         __syncthreads();
         return;
     }
