@@ -310,7 +310,7 @@ __device__ __forceinline__ uint2 cast4(float4 a) {
 // shard's values cast to bf16 or fp16 or copied as fp32 (kOut), zeros past the shard,
 // written to every destination.  Each thread handles 4 elements per sub-step
 // (16 bytes of fp32 in), so every load and store instruction of a wave covers
-// one contiguous run.
+// one contiguous run; the full tiles of a 16-bit push take 8 per thread.
 template <int kOut, class Dst>
 __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt) {
     constexpr bool kCast = kOut != kF32;
@@ -327,6 +327,27 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
     if (lo >= hi) return;
     // every destination chunk is 16-byte aligned, so one test covers them all
     const bool vec = is_aligned16(src) && is_aligned16(reinterpret_cast<Out*>(a.dst.at(0)) + off);
+    if constexpr (!kOne && kCast) {
+        // Pushed to W destinations, the stores outnumber the loads W to 1:
+        // each thread casts 8 consecutive elements and writes them with one
+        // 16-byte store per destination.
+        if (vec && hi - lo == kPackTile && lo + kPackTile <= valid) {
+            uint4 y[kPackSteps];
+#pragma unroll
+            for (int u = 0; u < kPackSteps; ++u) {
+                const float* s8 = src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 8;
+                const uint2 c0 = cast4<kOut>(ld16f(s8));
+                const uint2 c1 = cast4<kOut>(ld16f(s8 + 4));
+                y[u] = make_uint4(c0.x, c0.y, c1.x, c1.y);
+            }
+            for (int j = 0; j < ndst; ++j) {
+                Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
+#pragma unroll
+                for (int u = 0; u < kPackSteps; ++u) st16(dst + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 8, y[u]);
+            }
+            return;
+        }
+    }
     if (vec && hi - lo == kPackTile && lo + kPackTile <= valid) {
         float4 x[kSub];
 #pragma unroll
