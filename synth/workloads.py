@@ -52,6 +52,28 @@ def _block(key: int, name: str, world_size: int, dim: int, ffn: int, kv_rows: in
                     tuple(n.endswith("norm") for n in BLOCK_NAMES))
 
 
+def _block_tp(key: int, name: str, world_size: int, dim: int, ffn: int, kv_rows: int, tp: int) -> Workload:
+    """One block's tensor-parallel shards as an FSDP bucket on the data-parallel
+    sub-mesh (paper section 4, tensor parallel: each parameter is a 2-D DTensor
+    and the all-gather runs over the DP sub-mesh only; section 5 trains the 70B
+    model with TP degree 8).  The Megatron split: wq, wk, wv, w1 and w3 are
+    column-parallel (their output rows split over the TP group), wo and w2
+    row-parallel (their input columns split), the norm weights replicated."""
+    dims = (
+        (dim // tp, dim),        # wq
+        (kv_rows // tp, dim),    # wk
+        (kv_rows // tp, dim),    # wv
+        (dim, dim // tp),        # wo
+        (ffn // tp, dim),        # w1
+        (dim, ffn // tp),        # w2
+        (ffn // tp, dim),        # w3
+        (dim, 1),                # attention_norm
+        (dim, 1),                # ffn_norm
+    )
+    return Workload(key, name, world_size, BLOCK_NAMES, dims,
+                    tuple(n.endswith("norm") for n in BLOCK_NAMES))
+
+
 def _uneven(key: int) -> Workload:
     """Embedding, output projection, final norm and 37 odd-sized tensors.
 
@@ -74,6 +96,8 @@ WORKLOADS: dict[int, Workload] = {
     3: _block(3, "llama3-70b-block-w64", 64, dim=8192, ffn=28672, kv_rows=KV_ROWS),
     4: _block(4, "llama3-405b-block-w128", 128, dim=16384, ffn=53248, kv_rows=KV_ROWS),
     5: _uneven(5),
+    # 64 GPUs as TP 8 x DP 8: the bucket holds one TP rank's shards, W = 8
+    6: _block_tp(6, "llama3-70b-block-tp8-w8", 8, dim=8192, ffn=28672, kv_rows=KV_ROWS, tp=8),
 }
 
 

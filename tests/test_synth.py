@@ -16,7 +16,22 @@ def test_block_shapes_follow_llama31_table():
         assert d["wk"] == (1024, dim) and d["wv"] == (1024, dim)
         assert d["w1"] == (ffn, dim) and d["w3"] == (ffn, dim) and d["w2"] == (dim, ffn)
         assert d["attention_norm"] == (dim, 1) and d["ffn_norm"] == (dim, 1)
-    assert [w.world_size for w in WORKLOADS.values()] == [4, 8, 64, 128, 48]
+    assert [w.world_size for w in WORKLOADS.values()] == [4, 8, 64, 128, 48, 8]
+
+
+def test_tp_block_is_one_tp_rank_of_the_70b_block():
+    """Workload 6 holds one of 8 tensor-parallel ranks' shards of the 70B block:
+    8 of them make up workload 3's parameters (rows split for the column-parallel
+    weights, columns for the row-parallel ones, norms whole)."""
+    full = dict(zip(WORKLOADS[3].names, WORKLOADS[3].dims))
+    tp = dict(zip(WORKLOADS[6].names, WORKLOADS[6].dims))
+    for name in ("wq", "wk", "wv", "w1", "w3"):
+        assert (8 * tp[name][0], tp[name][1]) == full[name], name
+    for name in ("wo", "w2"):
+        assert (tp[name][0], 8 * tp[name][1]) == full[name], name
+    for name in ("attention_norm", "ffn_norm"):
+        assert tp[name] == full[name]
+    assert WORKLOADS[6].world_size == 8
 
 
 def test_uneven_workload():
@@ -63,7 +78,7 @@ def test_workload_sizes_match_the_worked_table():
         assert (wl.world_size, wl.num_params, wl.total_elems) == (W, P, E)
         plan = O.make_plan(W, wl.dims, 8)
         assert plan.chunk == S and W * S == WS
-        if key <= 4:
+        if key != 5:
             assert WS == E
         try:
             from paper_2411_00284_amd import BucketPlan
