@@ -18,8 +18,8 @@ import pytest
 import torch
 
 import oracle.fsdp_oracle as O
-from gpu_util import (DEV, Guarded, dev_random_bits16, dev_wide_f32, host_u16, host_u32, step, to_dev_f32,
-                      to_dev_u16)
+from gpu_util import (DEV, Guarded, dev_random_bits16, dev_wide_bf16, dev_wide_f32, host_u16, host_u32, step,
+                      to_dev_f32, to_dev_u16)
 from synth import WORKLOADS, random_bits16, random_bits32
 
 pytestmark = [pytest.mark.gpu,
@@ -294,3 +294,59 @@ def test_ex_workload_full(key):
     for p in range(P):
         assert np.array_equal(host_u32(outs[p]), want[p].reshape(-1).view(np.uint32)), p
     plan.close()
+
+
+def test_ex_workload_full_chunk_tables():
+    """The 70B block (W = 64) at full size through the W-pointer forms the
+    benchmark times: unpack pulling W chunks, rs_pack pushing into W chunks,
+    and the bf16 and fp16 reduces pulling W chunks."""
+    wl = WORKLOADS[3]
+    W = wl.world_size
+    plan = BucketPlan(W, wl.dims)
+    oplan = O.make_plan(W, wl.dims)
+    S = oplan.chunk
+    P = wl.num_params
+    # unpack from W chunks of random bf16 bit patterns
+    chunks = [dev_random_bits16(S, 900 + i) for i in range(W)]
+    params = [torch.empty(n * k, dtype=torch.bfloat16, device=DEV) for n, k in wl.dims]
+    step(f"ag_unpack_ex bf16 chunks full W={W}")
+    plan.ag_unpack_ex(chunks, params, "bf16")
+    torch.cuda.synchronize()
+    want = O.ag_unpack(oplan, np.concatenate([host_u16(c) for c in chunks]))
+    for p in range(P):
+        assert np.array_equal(host_u16(params[p]), want[p].reshape(-1)), p
+    del chunks, want
+    # rs_pack of the block's gradients into W chunks
+    grads = [dev_random_bits16(n * k, 950 + p) for p, (n, k) in enumerate(wl.dims)]
+    dsts = [torch.empty(S, dtype=torch.bfloat16, device=DEV) for _ in range(W)]
+    step(f"rs_pack_ex bf16 chunks full W={W}")
+    plan.rs_pack_ex(grads, dsts, "bf16")
+    torch.cuda.synchronize()
+    want = O.rs_pack(oplan, [host_u16(g).reshape(n, k) for g, (n, k) in zip(grads, wl.dims)])
+    for j in range(W):
+        assert np.array_equal(host_u16(dsts[j]), want[j * S:(j + 1) * S]), j
+    del grads, dsts, want, params
+    # bf16 reduce of rank W-1 from W chunks
+    recv = [dev_wide_bf16(S, 1000 + i) for i in range(W)]
+    outs = [torch.empty(O.local_elems(oplan, p, W - 1), dtype=torch.float32, device=DEV) for p in range(P)]
+    step(f"rs_reduce_ex bf16 chunks full W={W} rank={W - 1}")
+    plan.rs_reduce_ex(W - 1, recv, outs, "bf16")
+    torch.cuda.synchronize()
+    want = O.rs_reduce(oplan, W - 1, np.concatenate([host_u16(c) for c in recv]))
+    for p in range(P):
+        assert np.array_equal(host_u32(outs[p]), want[p].reshape(-1).view(np.uint32)), p
+    del recv, outs, want
+    # fp16 reduce of rank 0: finite fp16 values (exponent field below 16), W chunks
+    recv = [dev_random_bits16(S, 1100 + i) for i in range(W)]
+    for c in recv:
+        c.view(torch.int16).bitwise_and_(-0x4001)      # 0xBFFF: clears the exponent's top bit
+    outs = [torch.empty(O.local_elems(oplan, p, 0), dtype=torch.float32, device=DEV) for p in range(P)]
+    step(f"rs_reduce_ex f16 chunks full W={W} rank=0")
+    plan.rs_reduce_ex(0, [c.view(torch.float16) for c in recv], outs, "f16")
+    torch.cuda.synchronize()
+    want = O.rs_reduce(oplan, 0, np.concatenate([host_u16(c) for c in recv]).view(np.float16))
+    for p in range(P):
+        assert np.array_equal(host_u32(outs[p]), want[p].reshape(-1).view(np.uint32)), p
+    plan.close()
+    torch.cuda.empty_cache()
+
