@@ -64,10 +64,32 @@ def _rows_inner(shape) -> tuple[int, int]:
     return shape[0], math.prod(shape[1:]) if len(shape) > 1 else 1
 
 
-def _stream_handle(stream) -> int:
+def _stream_handle(stream, *groups) -> int:
+    """The HIP stream handle of ``stream`` (torch's current stream when None),
+    after checking that every non-empty tensor in ``groups`` lives on one
+    device, the stream's when the stream is a torch stream: the kernels
+    dereference every pointer on the device they run on."""
     if stream is None:
         stream = torch.cuda.current_stream()
-    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+    if hasattr(stream, "cuda_stream"):
+        handle, device = int(stream.cuda_stream), stream.device
+    else:
+        handle, device = int(stream), None
+    _check_device(device, groups)
+    return handle
+
+
+def _check_device(device, groups) -> None:
+    seen = device
+    for group in groups:
+        for t in group:
+            if t is None or t.numel() == 0:
+                continue
+            if seen is None:
+                seen = t.device
+            elif t.device != seen:
+                raise ValueError(f"a tensor on {t.device} where {seen} is expected: "
+                                 "one call's tensors and stream must share one device")
 
 
 def _ptr_array(tensors, expect_elems, dtypes, what) -> ctypes.Array:
@@ -156,21 +178,24 @@ class BucketPlan:
         arr = _ptr_array(shards, [self.local_elems(p, rank) for p in range(self.num_params)],
                          (torch.float32,), "shards")
         dst = _bucket_ptr(send_chunk, self.chunk_elems, BF16_DTYPES, "send_chunk")
-        _check(self._lib.fsdp_ag_pack(self._h, int(rank), arr, dst, _stream_handle(stream)), "fsdp_ag_pack")
+        h = _stream_handle(stream, shards, [send_chunk])
+        _check(self._lib.fsdp_ag_pack(self._h, int(rank), arr, dst, h), "fsdp_ag_pack")
 
     def ag_unpack(self, gathered: torch.Tensor, params: Sequence[torch.Tensor], stream=None) -> None:
         """Rank-major W*S bf16 buffer -> full bf16 parameters."""
         self._check_len(params, "params")
         src = _bucket_ptr(gathered, self.world_size * self.chunk_elems, BF16_DTYPES, "gathered")
         arr = _ptr_array(params, [self.full_elems(p) for p in range(self.num_params)], BF16_DTYPES, "params")
-        _check(self._lib.fsdp_ag_unpack(self._h, src, arr, _stream_handle(stream)), "fsdp_ag_unpack")
+        h = _stream_handle(stream, [gathered], params)
+        _check(self._lib.fsdp_ag_unpack(self._h, src, arr, h), "fsdp_ag_unpack")
 
     def rs_pack(self, grads: Sequence[torch.Tensor], send_buf: torch.Tensor, stream=None) -> None:
         """Full bf16 gradients -> destination-major W*S bf16 send buffer."""
         self._check_len(grads, "grads")
         arr = _ptr_array(grads, [self.full_elems(p) for p in range(self.num_params)], BF16_DTYPES, "grads")
         dst = _bucket_ptr(send_buf, self.world_size * self.chunk_elems, BF16_DTYPES, "send_buf")
-        _check(self._lib.fsdp_rs_pack(self._h, arr, dst, _stream_handle(stream)), "fsdp_rs_pack")
+        h = _stream_handle(stream, grads, [send_buf])
+        _check(self._lib.fsdp_rs_pack(self._h, arr, dst, h), "fsdp_rs_pack")
 
     def rs_reduce(self, rank: int, recv: torch.Tensor, grad_shards: Sequence[torch.Tensor], stream=None) -> None:
         """Source-major W*S bf16 buffer -> fp32 gradient shards of ``rank`` (average over ranks)."""
@@ -178,7 +203,8 @@ class BucketPlan:
         src = _bucket_ptr(recv, self.world_size * self.chunk_elems, BF16_DTYPES, "recv")
         arr = _ptr_array(grad_shards, [self.local_elems(p, rank) for p in range(self.num_params)],
                          (torch.float32,), "grad_shards")
-        _check(self._lib.fsdp_rs_reduce(self._h, int(rank), src, arr, _stream_handle(stream)), "fsdp_rs_reduce")
+        h = _stream_handle(stream, [recv], grad_shards)
+        _check(self._lib.fsdp_rs_reduce(self._h, int(rank), src, arr, h), "fsdp_rs_reduce")
 
     # ---- element-type and chunk-table forms
     def ag_pack_ex(self, rank: int, shards: Sequence[torch.Tensor], send_chunk: torch.Tensor,
@@ -189,7 +215,7 @@ class BucketPlan:
                          (torch.float32,), "shards")
         dst = _bucket_ptr(send_chunk, self.chunk_elems, _elem_dtypes(param_dtype), "send_chunk")
         _check(self._lib.fsdp_ag_pack_ex(self._h, int(rank), arr, _dtype_code(param_dtype), dst,
-                                         _stream_handle(stream)), "fsdp_ag_pack_ex")
+                                         _stream_handle(stream, shards, [send_chunk])), "fsdp_ag_pack_ex")
 
     def ag_pack_push(self, rank: int, shards: Sequence[torch.Tensor], chunks: Sequence[torch.Tensor],
                      param_dtype: str = "bf16", stream=None) -> None:
@@ -200,7 +226,7 @@ class BucketPlan:
                          (torch.float32,), "shards")
         carr = self._chunk_array(chunks, _elem_dtypes(param_dtype))
         _check(self._lib.fsdp_ag_pack_push(self._h, int(rank), arr, _dtype_code(param_dtype), carr,
-                                           _stream_handle(stream)), "fsdp_ag_pack_push")
+                                           _stream_handle(stream, shards, chunks)), "fsdp_ag_pack_push")
 
     def ag_unpack_ex(self, chunks: Sequence[torch.Tensor], params: Sequence[torch.Tensor],
                      param_dtype: str = "bf16", stream=None) -> None:
@@ -210,7 +236,7 @@ class BucketPlan:
         arr = _ptr_array(params, [self.full_elems(p) for p in range(self.num_params)],
                          _elem_dtypes(param_dtype), "params")
         _check(self._lib.fsdp_ag_unpack_ex(self._h, _dtype_code(param_dtype), carr, arr,
-                                           _stream_handle(stream)), "fsdp_ag_unpack_ex")
+                                           _stream_handle(stream, chunks, params)), "fsdp_ag_unpack_ex")
 
     def rs_pack_ex(self, grads: Sequence[torch.Tensor], chunks: Sequence[torch.Tensor],
                    reduce_dtype: str = "bf16", stream=None) -> None:
@@ -224,7 +250,7 @@ class BucketPlan:
         arr = _ptr_array(grads, [self.full_elems(p) for p in range(self.num_params)], _elem_dtypes(gname), "grads")
         carr = self._chunk_array(chunks, _elem_dtypes(reduce_dtype))
         _check(self._lib.fsdp_rs_pack_ex(self._h, _dtype_code(gname), arr, _dtype_code(reduce_dtype), carr,
-                                         _stream_handle(stream)), "fsdp_rs_pack_ex")
+                                         _stream_handle(stream, grads, chunks)), "fsdp_rs_pack_ex")
 
     def rs_reduce_ex(self, rank: int, chunks: Sequence[torch.Tensor], grad_shards: Sequence[torch.Tensor],
                      reduce_dtype: str = "bf16", stream=None) -> None:
@@ -234,7 +260,7 @@ class BucketPlan:
         arr = _ptr_array(grad_shards, [self.local_elems(p, rank) for p in range(self.num_params)],
                          (torch.float32,), "grad_shards")
         _check(self._lib.fsdp_rs_reduce_ex(self._h, int(rank), _dtype_code(reduce_dtype), carr, arr,
-                                           _stream_handle(stream)), "fsdp_rs_reduce_ex")
+                                           _stream_handle(stream, chunks, grad_shards)), "fsdp_rs_reduce_ex")
 
     def _chunk_array(self, chunks, dtypes) -> ctypes.Array:
         if len(chunks) != self.world_size:

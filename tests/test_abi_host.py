@@ -234,6 +234,19 @@ def test_binding_checks_tensors():
     plan.close()
 
 
+def test_binding_requires_one_device():
+    """One call's tensors (and its stream, when it is a torch stream) must share
+    a device: the kernels run on one device and dereference every pointer there."""
+    from paper_2411_00284_amd.bucket import _check_device
+    cpu, meta = torch.empty(3), torch.empty(3, device="meta")
+    _check_device(None, [[cpu, None, torch.empty(0, device="meta")], [cpu]])   # empty tensors are not read
+    _check_device(torch.device("cpu"), [[cpu], [cpu]])
+    with pytest.raises(ValueError):
+        _check_device(None, [[cpu], [meta]])
+    with pytest.raises(ValueError):
+        _check_device(torch.device("meta"), [[cpu]])
+
+
 @no_gpu
 def test_extended_calls_reject_bad_arguments():
     st_, h = raw_plan(4, [(5, 3), (8, 2)])
