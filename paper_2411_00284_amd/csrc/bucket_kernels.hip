@@ -8,7 +8,9 @@
 // parameter by parameter; the first tile of every parameter is kept in one
 // register per lane of a wavefront, and a ballot over it finds the parameter
 // of any tile in O(1).  The per-parameter table travels in the kernel
-// arguments, read through the scalar cache.
+// arguments, read through the scalar cache.  Tile counts fit in 31 bits (the
+// planner checks); grid-stride loops count in 64 bits so that the last step
+// cannot overflow.
 //
 // A bucket buffer of W chunks is addressed either as one allocation (chunk i
 // at base + i*stride) or through a table of W chunk pointers, so the same
@@ -392,7 +394,8 @@ template <int kOut, class Dst>
 __global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs<Dst> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
-    for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+    for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
+        const int t = int(step);
         const int p = param_of_tile(my_start, t);
         pack_tile<kOut>(a, p, t - a.tile_start[p]);
     }
@@ -418,7 +421,8 @@ template <class Chunks>
 __global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs<Chunks> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
-    for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+    for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
+        const int t = int(step);
         const int p = param_of_tile(my_start, t);
         const int lt = t - a.tile_start[p];
         const int tps = a.tiles_per_seg[p];
@@ -458,7 +462,8 @@ template <class Chunks, int kWiden>
 __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Chunks> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
-    for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+    for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
+        const int t = int(step);
         const int p = param_of_tile(my_start, t);
         const int lt = t - a.tile_start[p];
         const int tps = a.tiles_per_seg[p];
@@ -705,7 +710,8 @@ __global__ void __launch_bounds__(kReduceBlock) rs_reduce_kernel(const ReduceArg
     const int W = a.world;
     const float wf = float(W);
     const uint32_t t = threadIdx.x;
-    for (int tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+    for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
+        const int tile = int(step);
         const int p = param_of_tile(my_start, tile);
         const int64_t v = a.valid[p];
         const int64_t lo = int64_t(tile - a.tile_start[p]) * kReduceTile;
