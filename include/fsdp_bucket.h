@@ -41,9 +41,10 @@
  *     for fp32, 2 for bf16); unaligned ones take a slower element-wise path.
  *     A per-parameter pointer may be NULL only when it has no elements.
  *   - Outputs must not overlap inputs or each other (checked on the host).
- *   - A plan must outlive every launch that uses it only until the call
- *     returns (kernel arguments are copied at launch); plans are immutable
- *     and may be shared between threads and streams.
+ *   - A plan is needed only while a call runs: the kernel arguments are
+ *     copied at launch, so the plan may be freed once the call returns, even
+ *     with its launches still in flight.  Plans are immutable and may be
+ *     shared between threads and streams.
  *   - bf16 values are passed as uint16_t bit patterns.
  *   - A launch uses one workgroup per work tile, up to a per-device cap;
  *     past the cap every workgroup loops over several tiles.  The
