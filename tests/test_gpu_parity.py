@@ -225,6 +225,26 @@ def test_repeat_calls_are_identical():
         run_ag_pack(plan, oplan, 7, seed=3)
 
 
+def test_plan_freed_while_launches_are_in_flight():
+    """Kernel arguments are copied at launch: a plan freed right after the call
+    returns (before the GPU has run the kernel) leaves the result intact."""
+    w, dims = 8, [(20000, 64), (33, 1)]
+    oplan = O.make_plan(w, dims)
+    g = random_bits16([11, 1], w * oplan.chunk)
+    gathered = to_dev_u16(g)
+    outs = [torch.empty(n * k, dtype=torch.bfloat16, device=DEV) for n, k in dims]
+    torch.cuda.synchronize()
+    step("ag_unpack with the plan freed before the kernel runs")
+    torch.cuda._sleep(10_000_000)                 # keep the stream busy so the launch waits
+    plan = BucketPlan(w, dims)
+    plan.ag_unpack(gathered, outs)
+    plan.close()
+    torch.cuda.synchronize()
+    want = O.ag_unpack(oplan, g)
+    for p, o in enumerate(outs):
+        assert np.array_equal(host_u16(o), want[p].reshape(-1)), p
+
+
 # ----------------------------------------------------------------- full-size workloads
 
 def _full_ag_pack(plan, oplan, rank, seed):
