@@ -1,0 +1,42 @@
+"""The benchmark's one JSON line, from a short run on the toy block: the
+fields a reader of the line relies on are present and consistent."""
+
+from __future__ import annotations
+
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+import torch
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_bench_line_on_the_toy_block():
+    print("bench.py --workload 1 --steps 3 --warmup 1 --no-cpu-baseline", flush=True)
+    res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "1", "--steps", "3",
+                          "--warmup", "1", "--no-cpu-baseline", "--variant-reps", "1", "--event-every", "1"],
+                         capture_output=True, text=True, timeout=110)
+    assert res.returncode == 0, res.stderr[-2000:]
+    lines = [l for l in res.stdout.splitlines() if l.startswith("{")]
+    assert len(lines) == 1
+    d = json.loads(lines[0])
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+                "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "cpu_baseline", "kernels"):
+        assert key in d, key
+    assert d["n_gpus"] == 1 and d["steps"] == 3 and d["warmup"] == 1 and d["higher_is_better"] is True
+    assert d["config"]["workload"] == "toy-block-w4" and d["config"]["world_size"] == 4
+    step_bytes = sum(k["bytes"] for k in d["kernels"].values())
+    assert step_bytes == d["config"]["step_bytes"]
+    assert d["value"] > 0 and abs(d["value"] - step_bytes / (d["ms_per_step"] * 1e-3) / 1e9) < 0.01 * d["value"] + 0.2
+    r = d["roofline"]
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-3
+    assert d["cpu_baseline"] is None                 # skipped by the flag
+    assert set(d["kernels"]) == {"ag_pack", "ag_unpack", "rs_pack", "rs_reduce"}
+    assert d["d2d_copy"]["bytes"] == 2 * 2 * 4 * d["config"]["chunk_elems"]
