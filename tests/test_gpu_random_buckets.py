@@ -22,7 +22,10 @@ pytestmark = [pytest.mark.gpu,
 if torch.cuda.is_available():
     from paper_2411_00284_amd import BucketPlan
 
-N_CASES = 200
+import os
+
+# 200 by default; a longer sweep can ask for more (cases are seeded by index)
+N_CASES = int(os.environ.get("FSDP_TEST_RANDOM_CASES", "200"))
 
 
 def random_case(i):
