@@ -232,7 +232,7 @@ def main(argv=None):
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, rank)
+        cpu = cpu_baseline(wl, rank, gpu_plan=plan)
 
     ms_per_step = elapsed / args.steps * 1e3
     line = {
@@ -477,10 +477,13 @@ def fit_copy_cost(wl, stream, reps=5):
     return res
 
 
-def cpu_baseline(wl, rank=0, min_seconds=10.0, max_passes=50):
+def cpu_baseline(wl, rank=0, min_seconds=10.0, max_passes=50, gpu_plan=None):
     """The oracle, as it stands, timed on the host: all four steps at ``rank``
     over the whole bucket, repeated until about ``min_seconds`` of CPU work
-    has been measured (the oracle is single-threaded numpy)."""
+    has been measured (the oracle is single-threaded numpy).  With
+    ``gpu_plan`` (the library's plan of the same bucket) the four library
+    calls then run once on the same inputs and their outputs are compared with
+    the oracle's, bit for bit: the record's parity verdict."""
     import numpy as np
 
     import oracle.fsdp_oracle as O
@@ -500,11 +503,16 @@ def cpu_baseline(wl, rank=0, min_seconds=10.0, max_passes=50):
     t = {k: 0.0 for k in ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")}
     passes = 0
     while passes < max_passes and (passes == 0 or sum(t.values()) < min_seconds):
-        t0 = time.perf_counter(); O.ag_pack(plan, rank, shards); t["ag_pack"] += time.perf_counter() - t0
-        t0 = time.perf_counter(); O.ag_unpack(plan, gathered); t["ag_unpack"] += time.perf_counter() - t0
-        t0 = time.perf_counter(); O.rs_pack(plan, grads); t["rs_pack"] += time.perf_counter() - t0
-        t0 = time.perf_counter(); O.rs_reduce(plan, rank, recv); t["rs_reduce"] += time.perf_counter() - t0
+        t0 = time.perf_counter(); want_pack = O.ag_pack(plan, rank, shards); t["ag_pack"] += time.perf_counter() - t0
+        t0 = time.perf_counter(); want_unpack = O.ag_unpack(plan, gathered); t["ag_unpack"] += time.perf_counter() - t0
+        t0 = time.perf_counter(); want_send = O.rs_pack(plan, grads); t["rs_pack"] += time.perf_counter() - t0
+        t0 = time.perf_counter(); want_red = O.rs_reduce(plan, rank, recv); t["rs_reduce"] += time.perf_counter() - t0
         passes += 1
+    parity = None
+    if gpu_plan is not None:
+        parity = library_parity(gpu_plan, rank, shards, gathered, grads, recv,
+                                (want_pack, want_unpack, want_send, want_red))
+        del want_pack, want_unpack, want_send, want_red
     b = algorithmic_bytes(W, S, E, V0)
     total_s = sum(t.values())
     return {
@@ -517,7 +525,50 @@ def cpu_baseline(wl, rank=0, min_seconds=10.0, max_passes=50):
                    f"host has {len(os.sched_getaffinity(0))} cores"),
         "seconds": round(total_s, 3),
         "per_pass_s": {k: round(v / passes, 4) for k, v in t.items()},
+        "parity": parity,
     }
+
+
+def library_parity(plan, rank, shards, gathered, grads, recv, want):
+    """Each library call once on the oracle's inputs: does every output element
+    equal the oracle's, bit for bit?"""
+    import numpy as np
+    import torch
+
+    dev = torch.device("cuda:0")
+
+    def up16(a):
+        return torch.from_numpy(np.ascontiguousarray(a).reshape(-1).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    def down(t, dtype):
+        return t.view(torch.int16 if dtype == np.uint16 else torch.int32).cpu().numpy().view(dtype)
+
+    want_pack, want_unpack, want_send, want_red = want
+    P, S, W = plan.num_params, plan.chunk_elems, plan.world_size
+    res = {}
+    d_shards = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in shards]
+    out = torch.empty(S, dtype=torch.bfloat16, device=dev)
+    plan.ag_pack(rank, d_shards, out)
+    res["ag_pack"] = bool(np.array_equal(down(out, np.uint16), want_pack))
+    del d_shards, out
+    d_gathered = up16(gathered)
+    params = [torch.empty(plan.full_elems(p), dtype=torch.bfloat16, device=dev) for p in range(P)]
+    plan.ag_unpack(d_gathered, params)
+    res["ag_unpack"] = all(np.array_equal(down(params[p], np.uint16), want_unpack[p].reshape(-1)) for p in range(P))
+    del d_gathered, params
+    d_grads = [up16(g) for g in grads]
+    send = torch.empty(W * S, dtype=torch.bfloat16, device=dev)
+    plan.rs_pack(d_grads, send)
+    res["rs_pack"] = bool(np.array_equal(down(send, np.uint16), want_send))
+    del d_grads, send
+    d_recv = up16(recv)
+    outs = [torch.empty(plan.local_elems(p, rank), dtype=torch.float32, device=dev) for p in range(P)]
+    plan.rs_reduce(rank, d_recv, outs)
+    res["rs_reduce"] = all(np.array_equal(down(outs[p], np.uint32), want_red[p].reshape(-1).view(np.uint32))
+                           for p in range(P))
+    del d_recv, outs
+    torch.cuda.empty_cache()
+    return res
 
 
 if __name__ == "__main__":

@@ -18,9 +18,9 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def test_bench_line_on_the_toy_block():
-    print("bench.py --workload 1 --steps 3 --warmup 1 --no-cpu-baseline", flush=True)
+    print("bench.py --workload 1 --steps 3 --warmup 1", flush=True)
     res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "1", "--steps", "3",
-                          "--warmup", "1", "--no-cpu-baseline", "--variant-reps", "1", "--event-every", "1"],
+                          "--warmup", "1", "--variant-reps", "1", "--event-every", "1"],
                          capture_output=True, text=True, timeout=110)
     assert res.returncode == 0, res.stderr[-2000:]
     lines = [l for l in res.stdout.splitlines() if l.startswith("{")]
@@ -37,6 +37,9 @@ def test_bench_line_on_the_toy_block():
     r = d["roofline"]
     assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
     assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-3
-    assert d["cpu_baseline"] is None                 # skipped by the flag
+    cpu = d["cpu_baseline"]
+    assert cpu["kind"] == "oracle" and cpu["cores"] == 1 and cpu["value"] > 0
+    # the library on the oracle's own inputs, compared bit for bit inside the bench
+    assert cpu["parity"] == {"ag_pack": True, "ag_unpack": True, "rs_pack": True, "rs_reduce": True}
     assert set(d["kernels"]) == {"ag_pack", "ag_unpack", "rs_pack", "rs_reduce"}
     assert d["d2d_copy"]["bytes"] == 2 * 2 * 4 * d["config"]["chunk_elems"]
