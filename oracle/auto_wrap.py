@@ -29,7 +29,7 @@ Table 1):
   T^RS_m = alpha_RS + beta_RS * (RS words of B_{k-1}).
   Otherwise B is closed and node i starts the next bucket alone.
 
-Readings where the paper is silent (each also listed in the design notes):
+Readings where the paper is silent:
 
 * The first bucket's all-gather overlaps no computation: for B_0, T_c = 0.
   With alpha_AG > 0 it therefore holds one node.

@@ -27,7 +27,7 @@ What is computed (SimpleFSDP, arXiv 2411.00284):
   the bucket is reduce-scattered with averaging, and each rank reads its
   gradients out of the reduced buffer.
 
-Readings where the paper is silent (each also listed in the design notes):
+Readings where the paper is silent:
 
 * bucket layout: parameters in caller order; parameter p starts at off_p,
   a multiple of the alignment ``align`` (elements); each per-rank chunk has
