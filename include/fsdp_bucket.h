@@ -33,7 +33,7 @@
  *     caller owns every buffer and every host pointer array; the library owns
  *     only plans.  The hot calls allocate nothing, never synchronise, and
  *     enqueue exactly one kernel on `stream` (0 = the null stream), or none
- *     when there is nothing to write.
+ *     when there is nothing to write (the push at W >= 8: two).
  *   - All arguments are validated on the host before any HIP call; on any
  *     error nothing is enqueued and no output is touched.
  *   - Bucket buffers (send_chunk, gathered, send_buf, recv) must be 16-byte
@@ -221,7 +221,9 @@ fsdp_status fsdp_ag_pack_ex(const fsdp_plan* plan, int32_t rank, const float* co
  * where rank i receives this rank's chunk (slot `rank` of rank i's gathered
  * buffer), so the one-shot all-gather is fused with the copy-in.  Each of the
  * W chunks receives the same S elements of param_dtype; the shards are read
- * once.  The chunks must not overlap each other or the shards. */
+ * once.  The chunks must not overlap each other or the shards.  At W >= 8
+ * the call enqueues two kernels: the pack into chunks[rank], then its copy to
+ * the other W - 1 chunks (which reads chunks[rank] back); below 8, one. */
 fsdp_status fsdp_ag_pack_push(const fsdp_plan* plan, int32_t rank, const float* const* shards,
                               fsdp_dtype param_dtype, void* const* chunks, hipStream_t stream);
 

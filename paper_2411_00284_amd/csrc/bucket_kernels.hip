@@ -122,14 +122,14 @@ __device__ __forceinline__ uint4 ld16(const void* p) {
 #endif
     return make_uint4(v.x, v.y, v.z, v.w);
 }
+// Stores are non-temporal unless kNt is false: a chunk that other workgroups
+// read back at once (the first half of a wide push) is stored through the cache.
+template <bool kNt = bool(FSDP_NT_STORE)>
 __device__ __forceinline__ void st16(void* p, uint4 v) {
     u32x4* q = reinterpret_cast<u32x4*>(p);
     const u32x4 w = {v.x, v.y, v.z, v.w};
-#if FSDP_NT_STORE
-    __builtin_nontemporal_store(w, q);
-#else
-    *q = w;
-#endif
+    if constexpr (kNt) __builtin_nontemporal_store(w, q);
+    else *q = w;
 }
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
@@ -142,14 +142,12 @@ __device__ __forceinline__ uint2 ld8(const void* p) {
 #endif
     return make_uint2(v.x, v.y);
 }
+template <bool kNt = bool(FSDP_NT_STORE)>
 __device__ __forceinline__ void st8(void* p, uint2 v) {
     u32x2* q = reinterpret_cast<u32x2*>(p);
     const u32x2 w = {v.x, v.y};
-#if FSDP_NT_STORE
-    __builtin_nontemporal_store(w, q);
-#else
-    *q = w;
-#endif
+    if constexpr (kNt) __builtin_nontemporal_store(w, q);
+    else *q = w;
 }
 __device__ __forceinline__ float4 ld16f(const float* p) {
     const f32x4* q = reinterpret_cast<const f32x4*>(p);
@@ -160,14 +158,12 @@ __device__ __forceinline__ float4 ld16f(const float* p) {
 #endif
     return make_float4(v.x, v.y, v.z, v.w);
 }
+template <bool kNt = bool(FSDP_NT_STORE)>
 __device__ __forceinline__ void st16f(float* p, float4 v) {
     f32x4* q = reinterpret_cast<f32x4*>(p);
     const f32x4 w = {v.x, v.y, v.z, v.w};
-#if FSDP_NT_STORE
-    __builtin_nontemporal_store(w, q);
-#else
-    *q = w;
-#endif
+    if constexpr (kNt) __builtin_nontemporal_store(w, q);
+    else *q = w;
 }
 
 // ------------------------------------------------------------------ bucket chunk addressing
@@ -313,7 +309,7 @@ __device__ __forceinline__ uint2 cast4(float4 a) {
 // written to every destination.  Each thread handles 4 elements per sub-step
 // (16 bytes of fp32 in), so every load and store instruction of a wave covers
 // one contiguous run; the full tiles of a 16-bit push take 8 per thread.
-template <int kOut, class Dst>
+template <int kOut, class Dst, bool kNt = true>
 __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt) {
     constexpr bool kCast = kOut != kF32;
     typedef typename std::conditional<kCast, uint16_t, uint32_t>::type Out;
@@ -345,7 +341,7 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
             for (int j = 0; j < ndst; ++j) {
                 Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
 #pragma unroll
-                for (int u = 0; u < kPackSteps; ++u) st16(dst + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 8, y[u]);
+                for (int u = 0; u < kPackSteps; ++u) st16<kNt>(dst + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 8, y[u]);
             }
             return;
         }
@@ -359,8 +355,8 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
 #pragma unroll
             for (int u = 0; u < kSub; ++u) {
                 const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
-                if (kCast) st8(dst + g, cast4<kOut>(x[u]));
-                else st16f(reinterpret_cast<float*>(dst + g), x[u]);
+                if (kCast) st8<kNt>(dst + g, cast4<kOut>(x[u]));
+                else st16f<kNt>(reinterpret_cast<float*>(dst + g), x[u]);
             }
         }
         return;
@@ -372,8 +368,8 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
             const float4 x = g < valid ? ld16f(src + g) : make_float4(0.f, 0.f, 0.f, 0.f);
             for (int j = 0; j < ndst; ++j) {
                 Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
-                if (kCast) st8(dst + g, g < valid ? cast4<kOut>(x) : make_uint2(0, 0));
-                else st16(dst + g, g < valid ? make_uint4(__float_as_uint(x.x), __float_as_uint(x.y),
+                if (kCast) st8<kNt>(dst + g, g < valid ? cast4<kOut>(x) : make_uint2(0, 0));
+                else st16<kNt>(dst + g, g < valid ? make_uint4(__float_as_uint(x.x), __float_as_uint(x.y),
                                                           __float_as_uint(x.z), __float_as_uint(x.w))
                                              : make_uint4(0, 0, 0, 0));
             }
@@ -398,6 +394,66 @@ __global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs<Dst>
         const int t = int(step);
         const int p = param_of_tile(my_start, t);
         pack_tile<kOut>(a, p, t - a.tile_start[p]);
+    }
+}
+
+// The first half of a wide push: the rank's own chunk, stored through the
+// cache so that the copies to the other destinations read it back from L2 and
+// the MALL.  (Read back at once by many workgroups, a chunk just written with
+// non-temporal stores streamed at little more than half the rate.)
+template <int kOut>
+__global__ void __launch_bounds__(kCopyBlock) push_pack_kernel(const PackArgs<OneChunk> a) {
+    const int lane = threadIdx.x & 63;
+    const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
+    for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
+        const int t = int(step);
+        const int p = param_of_tile(my_start, t);
+        pack_tile<kOut, OneChunk, false>(a, p, t - a.tile_start[p]);
+    }
+}
+
+// The second half of a wide push: chunk `from` copied to the other W - 1
+// chunks of a table.  One work item is one tile of 16-byte units of one
+// destination.  Workgroups are dealt to the 8 XCDs round-robin (workgroup b
+// runs on XCD b mod 8; a grid-stride step is a multiple of 8), so the items are
+// numbered to put all destinations of a tile on one XCD: the tile is read into
+// that XCD's L2 once (cached loads) and written W - 1 times (non-temporal
+// stores), each workgroup writing one contiguous run.
+#ifndef FSDP_PUSH_REPLICATE_MIN_W
+#define FSDP_PUSH_REPLICATE_MIN_W 8
+#endif
+constexpr int kXcds = 8;
+constexpr int64_t kRepTile = kCopyBlock;          // 16-byte units per tile (2 KB)
+constexpr int kReplicateMinW = FSDP_PUSH_REPLICATE_MIN_W;
+
+struct ReplicateArgs {
+    TableChunks dst;
+    int64_t units;        // whole 16-byte units of a chunk
+    int32_t tail;         // 2-byte elements after them
+    int32_t from;         // the source chunk
+    int32_t ndst;         // W - 1 destinations
+    int32_t ntiles;
+    int32_t nitems;
+};
+
+__global__ void __launch_bounds__(kCopyBlock) replicate_kernel(const ReplicateArgs a) {
+    const u32x4* __restrict__ src = reinterpret_cast<const u32x4*>(a.dst.ptr[a.from]);
+    for (int64_t step = blockIdx.x; step < a.nitems; step += gridDim.x) {
+        const int i = int(step);
+        const int k = i / kXcds;
+        const int t = (k / a.ndst) * kXcds + i % kXcds;
+        if (t >= a.ntiles) continue;
+        int j = k % a.ndst;
+        j += j >= a.from;                            // every chunk but the source
+        u32x4* __restrict__ d = reinterpret_cast<u32x4*>(a.dst.ptr[j]);
+        const int64_t g = int64_t(t) * kRepTile + threadIdx.x;
+        if (g < a.units) {
+            __builtin_nontemporal_store(src[g], d + g);
+        } else if (g == a.units && a.tail > 0) {     // one thread copies the partial unit
+            const uint16_t* s2 = reinterpret_cast<const uint16_t*>(src + a.units);
+            uint16_t* d2 = reinterpret_cast<uint16_t*>(d + a.units);
+            for (int e = 0; e < a.tail; ++e) d2[e] = s2[e];
+        }
     }
 }
 
@@ -869,7 +925,7 @@ int64_t tiles(int64_t n, int64_t tile) { return (n + tile - 1) / tile; }
 // (TableChunks); `outs` holds their byte spans for the overlap check.
 template <class Dst>
 fsdp_status do_ag_pack(const Plan& pl, int32_t rank, const float* const* shards, fsdp_dtype wire, const Dst& dst,
-                       int ndst, const std::vector<Span>& outs, hipStream_t stream) {
+                       int ndst, const std::vector<Span>& outs, hipStream_t stream, bool cached = false) {
     fsdp_status st;
     if (rank < 0 || rank >= pl.world) return fail(FSDP_ERR_INVALID, "rank out of range");
     if (shards == nullptr) return fail(FSDP_ERR_INVALID, "shards is NULL");
@@ -893,6 +949,13 @@ fsdp_status do_ag_pack(const Plan& pl, int32_t rank, const float* const* shards,
     if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
     a.ntiles = int32_t(nt);
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
+    if constexpr (std::is_same<Dst, OneChunk>::value) {
+        if (cached) {
+            if (wire == FSDP_DTYPE_BF16) return launch(push_pack_kernel<kBF16>, a, a.ntiles, kCopyBlock, stream);
+            if (wire == FSDP_DTYPE_F16) return launch(push_pack_kernel<kF16>, a, a.ntiles, kCopyBlock, stream);
+            return launch(push_pack_kernel<kF32>, a, a.ntiles, kCopyBlock, stream);
+        }
+    }
     if (wire == FSDP_DTYPE_BF16) return launch(ag_pack_kernel<kBF16, Dst>, a, a.ntiles, kCopyBlock, stream);
     if (wire == FSDP_DTYPE_F16) return launch(ag_pack_kernel<kF16, Dst>, a, a.ntiles, kCopyBlock, stream);
     return launch(ag_pack_kernel<kF32, Dst>, a, a.ntiles, kCopyBlock, stream);
@@ -1040,12 +1103,32 @@ extern "C" fsdp_status fsdp_ag_pack_push(const fsdp_plan* h, int32_t rank, const
     const Plan* pl = get_plan(h, &st);
     if (!pl) return st;
     if (!known_dtype(param_dtype)) return fail(FSDP_ERR_INVALID, "unknown dtype");
+    if (rank < 0 || rank >= pl->world) return fail(FSDP_ERR_INVALID, "rank out of range");
+    const int esize = elem_bytes(param_dtype);
     TableChunks dst{};
     std::vector<Span> outs;
-    if ((st = load_chunk_table(*pl, const_cast<const void* const*>(chunks), elem_bytes(param_dtype), &dst, &outs)) !=
-        FSDP_OK)
+    if ((st = load_chunk_table(*pl, const_cast<const void* const*>(chunks), esize, &dst, &outs)) != FSDP_OK)
         return st;
-    return do_ag_pack(*pl, rank, shards, param_dtype, dst, pl->world, outs, stream);
+    if (pl->world < kReplicateMinW || pl->chunk == 0)
+        return do_ag_pack(*pl, rank, shards, param_dtype, dst, pl->world, outs, stream);
+    // Many destinations: pack once into the rank's own chunk (through the
+    // cache), then copy that chunk to the other W - 1.  Every chunk's span is
+    // in the overlap check of the pack.
+    ReplicateArgs r{};
+    r.dst = dst;
+    const int64_t bytes = pl->chunk * esize;
+    r.units = bytes / 16;
+    r.tail = int32_t(bytes % 16 / 2);
+    r.from = rank;
+    r.ndst = pl->world - 1;
+    const int64_t nt = tiles(r.units + (r.tail > 0), kRepTile);
+    const int64_t items = tiles(nt, kXcds) * kXcds * r.ndst;
+    if (items > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
+    r.ntiles = int32_t(nt);
+    r.nitems = int32_t(items);
+    if ((st = do_ag_pack(*pl, rank, shards, param_dtype, OneChunk{dst.ptr[rank]}, 1, outs, stream, true)) != FSDP_OK)
+        return st;
+    return launch(replicate_kernel, r, r.nitems, kCopyBlock, stream);
 }
 
 extern "C" fsdp_status fsdp_ag_unpack(const fsdp_plan* h, const uint16_t* gathered, uint16_t* const* params,

@@ -1,7 +1,7 @@
 """GPU parity on seeded random buckets: world sizes 1-128, 1-64 parameters
 of random shapes (empty, 1-wide, dim 0 below W, several tiles), every
 alignment 1-16, element-aligned parameter pointers, random ranks.  Every
-kernel and every element-type and chunk-table form is compared with the
+kernel and every element-type, chunk-table and push form is compared with the
 oracle bit for bit, inside poisoned guard bands."""
 
 from __future__ import annotations
@@ -161,4 +161,14 @@ def test_random_bucket(i):
     for p, q in enumerate(params):
         assert q.guards_intact(), p
         assert np.array_equal(host_u16(q.view), wantu[p].reshape(-1)), p
+    # the bf16 pack of rank r pushed to W separate destinations (at W >= 8 a
+    # pack into chunk r followed by a copy to the others)
+    dsts = [Guarded(S, torch.bfloat16) for _ in range(W)]
+    step(f"random bucket {i}: ag_pack_push bf16 to {W} chunks, rank {r}")
+    plan.ag_pack_push(r, [b.view for b in bufs], [d.view for d in dsts])
+    torch.cuda.synchronize()
+    wantp = O.ag_pack(oplan, r, shards)
+    for j, d in enumerate(dsts):
+        assert d.guards_intact(), j
+        assert np.array_equal(host_u16(d.view), wantp), j
     plan.close()
