@@ -66,6 +66,22 @@ def kernel_source_sha():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
+def read_profile_avg_us(kernel: str, workload: str):
+    """The kernel's average duration in the committed rocprofv3 summary of the
+    same workload, or None when there is none or the kernel source changed
+    since it was taken (event timing reads short kernels long; this is the
+    kernel's own duration)."""
+    path = os.path.join(PROFILES, f"kernels_{workload}_stats.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
+    if not m or m.group(1) != kernel_source_sha():
+        return None
+    m = re.search(rf"^\|\s*{kernel}\s*\|[^|]*\|[^|]*\|\s*([0-9.]+)\s*\|", text, re.M)
+    return float(m.group(1)) if m else None
+
+
 def read_traffic(kernel: str, workload: str):
     """HBM traffic per launch from the committed counter summary, or None when
     there is none or the kernel source changed since the counters were taken."""
@@ -201,7 +217,8 @@ def main(argv=None):
         kernels[name] = {"avg_us": round(avg_ms * 1e3, 2),
                          "median_us": round(float(np.median(per_kernel_ms[name])) * 1e3, 2),
                          "min_us": round(float(np.min(per_kernel_ms[name])) * 1e3, 2),
-                         "bytes": abytes[name], "GBps": round(gbps, 1), "frac": round(gbps / PEAK_GBPS, 4)}
+                         "bytes": abytes[name], "GBps": round(gbps, 1), "frac": round(gbps / PEAK_GBPS, 4),
+                         "rocprof_avg_us": read_profile_avg_us(name, wl.name)}
 
     copy_ref = None if args.no_variants else time_d2d_copy(gathered, send_buf, stream, args.variant_reps)
 
