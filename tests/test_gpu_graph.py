@@ -94,3 +94,43 @@ def test_step_replayed_from_a_graph(key):
             assert np.array_equal(host_u32(outs[p]), want[p].reshape(-1).view(np.uint32))
     del graph
     plan.close()
+
+
+@pytest.mark.parametrize("W", [4, 8, 48])
+def test_push_replayed_from_a_graph(W):
+    """The push (one kernel below W = 8, a pack and a copy from W = 8 on)
+    captured and replayed: every replay equals the eager push."""
+    dims = [(3 * W + 1, 64), (W + 3, 1), (5, 8)]
+    rank = W // 2
+    plan = BucketPlan(W, dims)
+    S = plan.chunk_elems
+    g = torch.Generator(device=DEV)
+    g.manual_seed(W)
+    shards = [torch.randn(plan.local_elems(p, rank), device=DEV, generator=g) for p in range(len(dims))]
+    dsts = [torch.empty(S, dtype=torch.bfloat16, device=DEV) for _ in range(W)]
+    step(f"graph: eager push W={W}")
+    plan.ag_pack_push(rank, shards, dsts)
+    torch.cuda.synchronize()
+    ref = [d.clone() for d in dsts]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        plan.ag_pack_push(rank, shards, dsts)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    step(f"graph: capture push W={W}")
+    with torch.cuda.graph(graph):
+        plan.ag_pack_push(rank, shards, dsts)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for d in dsts:
+            d.view(torch.uint8).fill_(0xFF)
+        torch.cuda.synchronize()
+        step(f"graph: replay {rep} push W={W}")
+        graph.replay()
+        torch.cuda.synchronize()
+        for j, (d, r) in enumerate(zip(dsts, ref)):
+            assert torch.equal(_bits(d), _bits(r)), (rep, j)
+    del graph
+    plan.close()
