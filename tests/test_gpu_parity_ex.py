@@ -212,6 +212,15 @@ def test_ex_grid_stride(cap, monkeypatch):
     test_ex_small(5, 8)
 
 
+@pytest.mark.parametrize("cap", [1, 7, 50])
+def test_push_grid_stride(cap, monkeypatch):
+    """The push at W = 48 (a pack and a copy) with every workgroup looping over
+    many work items, including caps that are not a multiple of the XCD count."""
+    monkeypatch.setenv("FSDP_MAX_WORKGROUPS", str(cap))
+    assert CASES[4][0] == 48
+    test_ag_pack_push(4)
+
+
 def test_ex_chunks_alias_one_buffer():
     """The chunk table may point into one [W][S] buffer: the results equal the
     contiguous calls bit for bit."""
