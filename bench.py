@@ -101,7 +101,7 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=3, help="1 toy, 2 8B, 3 70B (default), 4 405B, 5 uneven, 6 70B TP-8 shards")
+    ap.add_argument("--workload", type=int, default=3, help="1 toy, 2 8B, 3 70B (default), 4 405B, 5 uneven, 6 70B TP-8 shards, 7 8B at W=128")
     ap.add_argument("--rank", type=int, default=0, help="the rank whose share is timed (0 <= rank < W)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true",

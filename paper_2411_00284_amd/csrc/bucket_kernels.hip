@@ -500,7 +500,13 @@ __global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs<
 
 // Sizes in units of the source gradient: 2-byte units for a plain copy, 16-bit
 // elements when kWiden (kBF16 or kF16; kF32 = no widening) casts them to an
-// fp32 wire.
+// fp32 wire.  Tiles are numbered parameter by parameter and, within a
+// parameter, destination by destination; for W above kDestMajorW they are
+// numbered destination by destination and, within a destination, parameter by
+// parameter, so that the workgroups running at one time write one destination
+// chunk front to front instead of the segments of many chunks at once.
+constexpr int kDestMajorW = 64;
+
 template <class Chunks>
 struct RsPackArgs {
     const uint16_t* src[PMAX];   // full gradients
@@ -508,10 +514,12 @@ struct RsPackArgs {
     int64_t seg[PMAX];
     int64_t elems[PMAX];
     int32_t tiles_per_seg[PMAX]; // ceil((off_{p+1} - off_p) / tile)
-    int32_t tile_start[PMAX];
+    int32_t tile_start[PMAX];    // first tile of parameter p (within one destination if dest_major)
     Chunks dst;                  // send chunks, one per destination rank
     int32_t nparams;
-    int32_t ntiles;
+    int32_t dest_major;
+    int32_t tiles_per_dest;      // tiles of one destination chunk
+    int32_t ntiles;              // W * tiles_per_dest
 };
 
 template <class Chunks, int kWiden>
@@ -520,11 +528,19 @@ __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Ch
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
         const int t = int(step);
-        const int p = param_of_tile(my_start, t);
-        const int lt = t - a.tile_start[p];
-        const int tps = a.tiles_per_seg[p];
-        const int j = lt / tps;                          // destination rank
-        const int64_t st = lt - int64_t(j) * tps;
+        int p, j;                                        // parameter, destination rank
+        int64_t st;                                      // tile within the segment
+        if (a.dest_major) {
+            j = t / a.tiles_per_dest;
+            const int r = t - j * a.tiles_per_dest;
+            p = param_of_tile(my_start, r);
+            st = r - a.tile_start[p];
+        } else {
+            p = param_of_tile(my_start, t);
+            const int lt = t - a.tile_start[p];
+            j = lt / a.tiles_per_seg[p];
+            st = lt - int64_t(j) * a.tiles_per_seg[p];
+        }
         const int64_t region = a.off[p + 1] - a.off[p];
         const int64_t L = a.seg[p];
         const int64_t rest = a.elems[p] - int64_t(j) * L;
@@ -1026,17 +1042,21 @@ fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, cons
         a.seg[p] = pl.seg[p] * u;
         a.elems[p] = e * u;
         const int64_t tps = tiles((pl.off[p + 1] - pl.off[p]) * u, kWiden != kF32 ? kWidenTile : kCopyTile);
-        if (tps > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
+        if (tps * pl.world > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
         a.tiles_per_seg[p] = int32_t(tps);
-        a.tile_start[p] = int32_t(nt);
-        nt += int64_t(pl.world) * a.tiles_per_seg[p];
-        if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
+        a.tile_start[p] = int32_t(nt);                  // rescaled below for the parameter-major order
+        nt += tps;
+        if (nt * pl.world > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
         if (e > 0) ins.push_back(span(grads[p], e * gsize));
     }
+    a.dest_major = pl.world > kDestMajorW;
+    if (!a.dest_major)
+        for (int p = 0; p < pl.nparams; ++p) a.tile_start[p] *= pl.world;
     a.off[pl.nparams] = pl.chunk * u;
     a.dst = dst;
     a.nparams = pl.nparams;
-    a.ntiles = int32_t(nt);
+    a.tiles_per_dest = int32_t(nt);
+    a.ntiles = int32_t(nt * pl.world);
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
     return launch(rs_pack_kernel<Chunks, kWiden>, a, a.ntiles, kCopyBlock, stream);
 }

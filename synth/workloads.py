@@ -98,6 +98,8 @@ WORKLOADS: dict[int, Workload] = {
     5: _uneven(5),
     # 64 GPUs as TP 8 x DP 8: the bucket holds one TP rank's shards, W = 8
     6: _block_tp(6, "llama3-70b-block-tp8-w8", 8, dim=8192, ffn=28672, kv_rows=KV_ROWS, tp=8),
+    # the 8B block under FSDP alone on 128 GPUs (the largest FSDP-only setting of section 5)
+    7: _block(7, "llama3-8b-block-w128", 128, dim=4096, ffn=14336, kv_rows=KV_ROWS),
 }
 
 

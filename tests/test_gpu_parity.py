@@ -300,7 +300,7 @@ def _full_rs_reduce(plan, oplan, rank, seed):
         assert np.array_equal(host_u32(o.view), want[p].reshape(-1).view(np.uint32)), p
 
 
-@pytest.mark.parametrize("key", [1, 2, 3, 5, 6])
+@pytest.mark.parametrize("key", [1, 2, 3, 5, 6, 7])
 @pytest.mark.parametrize("kernel", ["ag_pack", "ag_unpack", "rs_pack", "rs_reduce"])
 def test_workload_full(key, kernel):
     wl = WORKLOADS[key]

@@ -40,7 +40,7 @@ def run_all_checks(impl, quick=False):
     C.check_plan_toy_table(impl)
     C.check_plan_sharding_matches_torch_chunk(impl, SMALL_CASES)
     C.check_plan_invariants(impl, SMALL_CASES)
-    C.check_plan_even_workloads(impl, [WORKLOADS[k] for k in (1, 2, 3, 4, 6)])
+    C.check_plan_even_workloads(impl, [WORKLOADS[k] for k in (1, 2, 3, 4, 6, 7)])
     for w, dims in SMALL_CASES[:6]:
         for r in sorted({0, w // 2, w - 1}):
             C.check_ag_pack_bruteforce(impl, w, dims, r, seed=w)

@@ -8,7 +8,7 @@ from synth import WORKLOADS, grad_rows_bits, param_rows, random_bits16
 
 def test_block_shapes_follow_llama31_table():
     table = {r[0]: (int(r[2]), int(r[3])) for r in read_table("llama31_table2.txt")}
-    for key, model in ((2, "8B"), (3, "70B"), (4, "405B")):
+    for key, model in ((2, "8B"), (3, "70B"), (4, "405B"), (7, "8B")):
         dim, ffn = table[model]
         wl = WORKLOADS[key]
         d = dict(zip(wl.names, wl.dims))
@@ -16,7 +16,7 @@ def test_block_shapes_follow_llama31_table():
         assert d["wk"] == (1024, dim) and d["wv"] == (1024, dim)
         assert d["w1"] == (ffn, dim) and d["w3"] == (ffn, dim) and d["w2"] == (dim, ffn)
         assert d["attention_norm"] == (dim, 1) and d["ffn_norm"] == (dim, 1)
-    assert [w.world_size for w in WORKLOADS.values()] == [4, 8, 64, 128, 48, 8]
+    assert [w.world_size for w in WORKLOADS.values()] == [4, 8, 64, 128, 48, 8, 128]
 
 
 def test_tp_block_is_one_tp_rank_of_the_70b_block():
