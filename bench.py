@@ -40,12 +40,13 @@ METRIC = "effective HBM GB/s (and % of peak) for bucket pack/unpack/reduce"
 PEAK_GBPS = 8000.0                       # MI355X HBM3E
 KERNELS = ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")
 # device symbols of the kernels each call launches (bf16 wire, one contiguous
-# buffer); rocprofv3 reports them by these names
+# buffer); rocprofv3 reports them by these names.  A small rank shard (fewer
+# than 4 full-size tiles per CU) reduces with 128-thread workgroups instead.
 KERNEL_SYMBOLS = {
     "ag_pack": "ag_pack_kernel<1, OneChunk>",
     "ag_unpack": "ag_unpack_kernel<ContigChunks>",
     "rs_pack": "rs_pack_kernel<ContigChunks, 0>",
-    "rs_reduce": "rs_reduce_kernel<ContigChunks, unsigned short>",
+    "rs_reduce": "rs_reduce_kernel<ContigChunks, unsigned short, 256>",
 }
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_00284_amd", "csrc", "bucket_kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")

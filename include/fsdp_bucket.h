@@ -50,6 +50,9 @@
  *     past the cap every workgroup loops over several tiles.  The
  *     environment variable FSDP_MAX_WORKGROUPS, when it holds a positive
  *     count, lowers that cap (read at every launch; results do not change).
+ *   - The reduction cuts a small shard (fewer than 4 full-size tiles per CU)
+ *     into half-size tiles; FSDP_REDUCE_HALF_TILES=0 or 1 forces full- or
+ *     half-size tiles (read at every launch; results do not change).
  */
 #ifndef FSDP_BUCKET_H
 #define FSDP_BUCKET_H

@@ -587,21 +587,20 @@ __device__ __forceinline__ void init8(float (&acc)[8], uint4 x) {
     acc[6] = bf16_lo(x.w); acc[7] = bf16_hi(x.w);
 }
 
-// One thread's 8 values of a tile row (kReduceBlock * 8 elements) of one
+// One thread's 8 values of a tile row (kB * 8 elements, kB threads) of one
 // source, as loaded.  bf16 sources: elements [8t, 8t+8) of the row, one
-// 16-byte load.  fp32 sources: elements [4t, 4t+4) and [4B + 4t, 4B + 4t + 4)
-// (B = kReduceBlock), two 16-byte loads that each cover one contiguous run
-// across the wave.  Addresses are a wave-uniform row pointer plus a 32-bit
-// byte offset.
-template <typename T> struct Raw8;
-template <> struct Raw8<uint16_t> {
+// 16-byte load.  fp32 sources: elements [4t, 4t+4) and [4kB + 4t, 4kB + 4t + 4),
+// two 16-byte loads that each cover one contiguous run across the wave.
+// Addresses are a wave-uniform row pointer plus a 32-bit byte offset.
+template <typename T, int kB> struct Raw8;
+template <int kB> struct Raw8<uint16_t, kB> {
     uint4 x;
     __device__ __forceinline__ static uint32_t pos(uint32_t t, int e) { return t * 8 + e; }
     __device__ __forceinline__ void load(const uint16_t* row, uint32_t t) { x = ld16(row + t * 8); }
     __device__ __forceinline__ void init(float (&acc)[8]) const { init8(acc, x); }
     __device__ __forceinline__ void add(float (&acc)[8]) const { add8(acc, x); }
 };
-template <> struct Raw8<_Float16> {
+template <int kB> struct Raw8<_Float16, kB> {
     uint4 x;
     __device__ __forceinline__ static uint32_t pos(uint32_t t, int e) { return t * 8 + e; }
     __device__ __forceinline__ void load(const _Float16* row, uint32_t t) { x = ld16(row + t * 8); }
@@ -614,14 +613,14 @@ template <> struct Raw8<_Float16> {
         acc[4] += f16_lo(x.z); acc[5] += f16_hi(x.z); acc[6] += f16_lo(x.w); acc[7] += f16_hi(x.w);
     }
 };
-template <> struct Raw8<float> {
+template <int kB> struct Raw8<float, kB> {
     float4 a, b;
     __device__ __forceinline__ static uint32_t pos(uint32_t t, int e) {
-        return e < 4 ? t * 4 + e : uint32_t(kReduceBlock) * 4 + t * 4 + (e - 4);
+        return e < 4 ? t * 4 + e : uint32_t(kB) * 4 + t * 4 + (e - 4);
     }
     __device__ __forceinline__ void load(const float* row, uint32_t t) {
         a = ld16f(row + t * 4);
-        b = ld16f(row + uint32_t(kReduceBlock) * 4 + t * 4);
+        b = ld16f(row + uint32_t(kB) * 4 + t * 4);
     }
     __device__ __forceinline__ void init(float (&acc)[8]) const {
         acc[0] = a.x; acc[1] = a.y; acc[2] = a.z; acc[3] = a.w;
@@ -633,13 +632,13 @@ template <> struct Raw8<float> {
     }
 };
 
-// Store the 8 averages of thread t at the positions Raw8<T>::pos gives.
-template <typename T>
+// Store the 8 averages of thread t at the positions Raw8<T, kB>::pos gives.
+template <typename T, int kB>
 __device__ __forceinline__ void store_avg8(float* row, uint32_t t, const float (&acc)[8], float wf) {
     const float4 lo = make_float4(acc[0] / wf, acc[1] / wf, acc[2] / wf, acc[3] / wf);
     const float4 hi = make_float4(acc[4] / wf, acc[5] / wf, acc[6] / wf, acc[7] / wf);
-    st16f(row + Raw8<T>::pos(t, 0), lo);
-    st16f(row + Raw8<T>::pos(t, 4), hi);
+    st16f(row + Raw8<T, kB>::pos(t, 0), lo);
+    st16f(row + Raw8<T, kB>::pos(t, 4), hi);
 }
 
 // Typed pointer to the tile of source i: through the chunk table, or as a
@@ -656,10 +655,10 @@ __device__ __forceinline__ const T* source(const StridedTile<T>& c, int64_t off,
 // Loads of sources i0 .. i0+kReduceBatch-1 (those below W unless kFull) of a
 // full tile; all are issued before any of them is used.  `off` is the tile's
 // element offset inside every chunk.
-template <bool kFull, typename T, class Src>
-__device__ __forceinline__ void load_sources(Raw8<T> (&x)[kReduceBatch][kReduceSteps], const Src& src,
+template <bool kFull, typename T, int kB, class Src>
+__device__ __forceinline__ void load_sources(Raw8<T, kB> (&x)[kReduceBatch][kReduceSteps], const Src& src,
                                              int64_t off, int i0, int W, uint32_t t) {
-    constexpr uint32_t kRow = uint32_t(kReduceBlock) * kVec;
+    constexpr uint32_t kRow = uint32_t(kB) * kVec;
 #pragma unroll
     for (int b = 0; b < kReduceBatch; ++b) {
         if (kFull || i0 + b < W) {
@@ -673,13 +672,13 @@ __device__ __forceinline__ void load_sources(Raw8<T> (&x)[kReduceBatch][kReduceS
 // A full tile of kReduceSteps rows.  The W sources of every output are added
 // in rank order 0..W-1, starting from source 0; the loads of kReduceBatch
 // sources are issued ahead of their adds.
-template <typename T, class Src>
+template <typename T, int kB, class Src>
 __device__ __forceinline__ void reduce_tile_vec(const Src& src, int64_t off, float* __restrict__ dtile,
                                                 int W, float wf) {
-    constexpr uint32_t kRow = uint32_t(kReduceBlock) * kVec;
+    constexpr uint32_t kRow = uint32_t(kB) * kVec;
     const uint32_t t = threadIdx.x;
     float acc[kReduceSteps][8];
-    Raw8<T> x[kReduceBatch][kReduceSteps];
+    Raw8<T, kB> x[kReduceBatch][kReduceSteps];
     if (W >= kReduceBatch) load_sources<true>(x, src, off, 0, W, t);
     else load_sources<false>(x, src, off, 0, W, t);
 #pragma unroll
@@ -710,23 +709,23 @@ __device__ __forceinline__ void reduce_tile_vec(const Src& src, int64_t off, flo
     if constexpr (sizeof(T) == 2) {
         // Thread t holds outputs [8t, 8t + 8) of each row: staged through LDS
         // so that every store instruction of a wave covers one contiguous run.
-        __shared__ float4 stage[kReduceSteps * kReduceBlock * 2];
+        __shared__ float4 stage[kReduceSteps * kB * 2];
 #pragma unroll
         for (int u = 0; u < kReduceSteps; ++u) {
-            stage[(u * kReduceBlock + t) * 2] = make_float4(acc[u][0] / wf, acc[u][1] / wf, acc[u][2] / wf, acc[u][3] / wf);
-            stage[(u * kReduceBlock + t) * 2 + 1] = make_float4(acc[u][4] / wf, acc[u][5] / wf, acc[u][6] / wf, acc[u][7] / wf);
+            stage[(u * kB + t) * 2] = make_float4(acc[u][0] / wf, acc[u][1] / wf, acc[u][2] / wf, acc[u][3] / wf);
+            stage[(u * kB + t) * 2 + 1] = make_float4(acc[u][4] / wf, acc[u][5] / wf, acc[u][6] / wf, acc[u][7] / wf);
         }
         __syncthreads();
 #pragma unroll
         for (int u = 0; u < kReduceSteps; ++u)
 #pragma unroll
             for (int h = 0; h < 2; ++h)
-                st16f(dtile + u * kRow + (h * kReduceBlock + t) * 4, stage[u * kReduceBlock * 2 + h * kReduceBlock + t]);
+                st16f(dtile + u * kRow + (h * kB + t) * 4, stage[u * kB * 2 + h * kB + t]);
         __syncthreads();
         return;
     }
 #pragma unroll
-    for (int u = 0; u < kReduceSteps; ++u) store_avg8<T>(dtile + u * kRow, t, acc[u], wf);
+    for (int u = 0; u < kReduceSteps; ++u) store_avg8<T, kB>(dtile + u * kRow, t, acc[u], wf);
 }
 
 __device__ __forceinline__ float widen(uint16_t x) { return bf16_lo(x); }
@@ -736,11 +735,11 @@ __device__ __forceinline__ float widen(float x) { return x; }
 // One thread's group of 8 outputs of one row whose group lies wholly inside
 // the shard (partial tiles): the same rank-ordered sum, loads issued
 // kReduceBatch sources ahead.
-template <typename T, class Src>
+template <typename T, int kB, class Src>
 __device__ __forceinline__ void reduce_group_vec(const Src& src, int64_t off, float* __restrict__ drow, int W,
                                                  float wf, uint32_t t) {
     float acc[8];
-    Raw8<T> x[kReduceBatch];
+    Raw8<T, kB> x[kReduceBatch];
     for (int i = 0; i < W; i += kReduceBatch) {
 #pragma unroll
         for (int b = 0; b < kReduceBatch; ++b)
@@ -752,7 +751,7 @@ __device__ __forceinline__ void reduce_group_vec(const Src& src, int64_t off, fl
             else x[b].add(acc);
         }
     }
-    store_avg8<T>(drow, t, acc, wf);
+    store_avg8<T, kB>(drow, t, acc, wf);
 }
 
 // One output element at element offset `g` of every chunk (unaligned or
@@ -774,9 +773,12 @@ __device__ __forceinline__ float reduce_one(const Src& src, int64_t g, int W, fl
     return acc / wf;
 }
 
-template <class Chunks, typename T>
-__global__ void __launch_bounds__(kReduceBlock) rs_reduce_kernel(const ReduceArgs<Chunks> a) {
-    constexpr int64_t kRow = int64_t(kReduceBlock) * kVec;
+// kB threads per workgroup, each owning kReduceSteps groups of 8 outputs: a
+// tile of kB * 8 * kReduceSteps outputs.
+template <class Chunks, typename T, int kB>
+__global__ void __launch_bounds__(kB) rs_reduce_kernel(const ReduceArgs<Chunks> a) {
+    constexpr int64_t kRow = int64_t(kB) * kVec;
+    constexpr int64_t kTile = kRow * kReduceSteps;
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
     const int W = a.world;
@@ -786,18 +788,18 @@ __global__ void __launch_bounds__(kReduceBlock) rs_reduce_kernel(const ReduceArg
         const int tile = int(step);
         const int p = param_of_tile(my_start, tile);
         const int64_t v = a.valid[p];
-        const int64_t lo = int64_t(tile - a.tile_start[p]) * kReduceTile;
+        const int64_t lo = int64_t(tile - a.tile_start[p]) * kTile;
         const int64_t off = a.off[p];
         float* __restrict__ d0 = a.dst[p];
         const bool vec = is_aligned16(d0) && a.src.aligned() && ((off * int64_t(sizeof(T))) & 15) == 0;
-        if (vec && lo + kReduceTile <= v) {
+        if (vec && lo + kTile <= v) {
             if (std::is_same<Chunks, ContigChunks>::value) {
                 const ContigChunks& c = reinterpret_cast<const ContigChunks&>(a.src);
                 const StridedTile<T> st{reinterpret_cast<const T*>(c.base) + off + lo,
                                         c.stride / int64_t(sizeof(T))};
-                reduce_tile_vec<T>(st, 0, d0 + lo, W, wf);
+                reduce_tile_vec<T, kB>(st, 0, d0 + lo, W, wf);
             } else {
-                reduce_tile_vec<T>(reinterpret_cast<const TableChunks&>(a.src), off + lo, d0 + lo, W, wf);
+                reduce_tile_vec<T, kB>(reinterpret_cast<const TableChunks&>(a.src), off + lo, d0 + lo, W, wf);
             }
             continue;
         }
@@ -805,19 +807,19 @@ __global__ void __launch_bounds__(kReduceBlock) rs_reduce_kernel(const ReduceArg
         for (int u = 0; u < kReduceSteps; ++u) {
             const int64_t row = lo + u * kRow;
             if (row >= v) break;
-            if (vec && row + Raw8<T>::pos(t, 7) < v) {
+            if (vec && row + Raw8<T, kB>::pos(t, 7) < v) {
                 if (std::is_same<Chunks, ContigChunks>::value) {
                     const ContigChunks& c = reinterpret_cast<const ContigChunks&>(a.src);
                     const StridedTile<T> st{reinterpret_cast<const T*>(c.base) + off + row,
                                             c.stride / int64_t(sizeof(T))};
-                    reduce_group_vec<T>(st, 0, d0 + row, W, wf, t);
+                    reduce_group_vec<T, kB>(st, 0, d0 + row, W, wf, t);
                 } else {
-                    reduce_group_vec<T>(reinterpret_cast<const TableChunks&>(a.src), off + row, d0 + row, W, wf, t);
+                    reduce_group_vec<T, kB>(reinterpret_cast<const TableChunks&>(a.src), off + row, d0 + row, W, wf, t);
                 }
                 continue;
             }
             for (int e = 0; e < kVec; ++e) {
-                const int64_t g = row + Raw8<T>::pos(t, e);
+                const int64_t g = row + Raw8<T, kB>::pos(t, e);
                 if (g >= v) continue;
                 if (std::is_same<Chunks, ContigChunks>::value) {
                     const ContigChunks& c = reinterpret_cast<const ContigChunks&>(a.src);
@@ -832,6 +834,9 @@ __global__ void __launch_bounds__(kReduceBlock) rs_reduce_kernel(const ReduceArg
 }
 
 // ------------------------------------------------------------------ host side
+
+// Below this many full-size reduce tiles per CU, the reduce uses half-size tiles.
+constexpr int kSmallShardTilesPerCU = 4;
 
 int cu_count(fsdp_status* st) {
     static std::atomic<int> cache[64];
@@ -1066,8 +1071,30 @@ fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, cons
 template <class Chunks, typename T>
 fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const std::vector<Span>& ins,
                          float* const* grad_shards, hipStream_t stream) {
-    fsdp_status st;
+    fsdp_status st = FSDP_OK;
     if (grad_shards == nullptr) return fail(FSDP_ERR_INVALID, "grad_shards is NULL");
+    std::vector<Span> outs;
+    int64_t full_tiles = 0;
+    for (int p = 0; p < pl.nparams; ++p) {
+        const int64_t v = pl.local_elems(p, rank);
+        if ((st = check_param_ptr(grad_shards[p], v, 4, p, "grad_shards")) != FSDP_OK) return st;
+        if (v > 0) outs.push_back(span(grad_shards[p], v * 4));
+        full_tiles += tiles(v, kReduceTile);
+    }
+    if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
+    if (full_tiles == 0) return FSDP_OK;                 // nothing to write: no launch
+    // A rank's shard that makes fewer than kSmallShardTilesPerCU full-size
+    // tiles per CU is cut into half-size tiles (half as many threads per
+    // workgroup, the same work per thread), so that the workgroups spread
+    // evenly over the CUs.  (The first HIP call: every argument is checked.)
+    const int cus = cu_count(&st);
+    if (st != FSDP_OK) return st;
+    bool small = full_tiles < int64_t(kSmallShardTilesPerCU) * cus;
+    if (const char* env = std::getenv("FSDP_REDUCE_HALF_TILES")) {   // "0" or "1" forces the choice
+        if (env[0] == '0') small = false;
+        if (env[0] == '1') small = true;
+    }
+    const int64_t tile = small ? kReduceTile / 2 : kReduceTile;
     // Tiles of the parameters with the fewest tiles are numbered (and so
     // dispatched) first: a ragged last tile sums its W sources in a longer
     // dependent chain, which then overlaps the bulk instead of trailing it.
@@ -1075,30 +1102,26 @@ fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const 
     std::vector<int64_t> nts(pl.nparams);
     for (int p = 0; p < pl.nparams; ++p) {
         order[p] = p;
-        nts[p] = tiles(pl.local_elems(p, rank), kReduceTile);
+        nts[p] = tiles(pl.local_elems(p, rank), tile);
     }
     std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return nts[x] < nts[y]; });
     ReduceArgs<Chunks> a{};
-    std::vector<Span> outs;
-    int64_t nt = 0;   // at most the planner's checked reduce tile count
+    int64_t nt = 0;
     for (int q = 0; q < pl.nparams; ++q) {
         const int p = order[q];
-        const int64_t v = pl.local_elems(p, rank);
-        if ((st = check_param_ptr(grad_shards[p], v, 4, p, "grad_shards")) != FSDP_OK) return st;
         a.dst[q] = grad_shards[p];
         a.off[q] = pl.off[p];
-        a.valid[q] = v;
+        a.valid[q] = pl.local_elems(p, rank);
         a.tile_start[q] = int32_t(nt);
         nt += nts[p];
-        if (v > 0) outs.push_back(span(grad_shards[p], v * 4));
+        if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
     }
     a.src = src;
     a.world = pl.world;
     a.nparams = pl.nparams;
-    if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
     a.ntiles = int32_t(nt);
-    if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    return launch(rs_reduce_kernel<Chunks, T>, a, a.ntiles, kReduceBlock, stream);
+    if (small) return launch(rs_reduce_kernel<Chunks, T, kReduceBlock / 2>, a, a.ntiles, kReduceBlock / 2, stream);
+    return launch(rs_reduce_kernel<Chunks, T, kReduceBlock>, a, a.ntiles, kReduceBlock, stream);
 }
 
 }  // namespace

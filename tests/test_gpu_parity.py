@@ -123,6 +123,22 @@ def wide_bf16_host(words, n):
 
 # ----------------------------------------------------------------- small buckets
 
+@pytest.mark.parametrize("half", ["0", "1"])
+def test_reduce_tile_sizes(half, monkeypatch):
+    """The reduction with its tile size forced each way (full-size tiles of 256
+    threads, half-size tiles of 128) on the small buckets, which otherwise
+    take the half-size tiles: every output bit for bit."""
+    monkeypatch.setenv("FSDP_REDUCE_HALF_TILES", half)
+    for case in range(len(SMALL)):
+        w, dims = SMALL[case]
+        plan = BucketPlan(w, dims)
+        oplan = O.make_plan(w, dims)
+        recv = wide_bf16_host([case, 77], w * oplan.chunk)
+        for r in _ranks(w):
+            run_rs_reduce(plan, oplan, r, recv)
+        plan.close()
+
+
 @pytest.mark.parametrize("cap", [1, 3, 50])
 @pytest.mark.parametrize("case", [3, 8, 10, 11])
 def test_grid_stride(case, cap, monkeypatch):
