@@ -417,14 +417,21 @@ __global__ void __launch_bounds__(kCopyBlock) push_pack_kernel(const PackArgs<On
 // destination.  Workgroups are dealt to the 8 XCDs round-robin (workgroup b
 // runs on XCD b mod 8; a grid-stride step is a multiple of 8), so the items are
 // numbered to put all destinations of a tile on one XCD: the tile is read into
-// that XCD's L2 once (cached loads) and written W - 1 times (non-temporal
-// stores), each workgroup writing one contiguous run.
+// that XCD's L2 once (cached loads) and written to each destination
+// (non-temporal stores), each workgroup writing one contiguous run.
+//
+// From kRepGroup destinations up, they are copied in groups of kRepGroup,
+// one group per grid row (blockIdx.y).  Workgroups are dispatched row by row,
+// so the workgroups in flight write long runs into few destinations instead
+// of short runs into all W - 1; the chunk is read once per group.
 #ifndef FSDP_PUSH_REPLICATE_MIN_W
 #define FSDP_PUSH_REPLICATE_MIN_W 8
 #endif
 constexpr int kXcds = 8;
 constexpr int64_t kRepTile = kCopyBlock;          // 16-byte units per tile (2 KB)
 constexpr int kReplicateMinW = FSDP_PUSH_REPLICATE_MIN_W;
+constexpr int kRepGroupLog2 = 4;
+constexpr int kRepGroup = 1 << kRepGroupLog2;     // destinations per grid row
 
 struct ReplicateArgs {
     TableChunks dst;
@@ -436,6 +443,22 @@ struct ReplicateArgs {
     int32_t nitems;
 };
 
+// Tile t of the source to destination index j (0 .. ndst-1, skipping `from`).
+__device__ __forceinline__ void replicate_tile(const ReplicateArgs& a, const u32x4* __restrict__ src, int t, int j) {
+    j += j >= a.from;                                // every chunk but the source
+    u32x4* __restrict__ d = reinterpret_cast<u32x4*>(a.dst.ptr[j]);
+    const int64_t g = int64_t(t) * kRepTile + threadIdx.x;
+    if (g < a.units) {
+        __builtin_nontemporal_store(src[g], d + g);
+    } else if (g == a.units && a.tail > 0) {         // one thread copies the partial unit
+        const uint16_t* s2 = reinterpret_cast<const uint16_t*>(src + a.units);
+        uint16_t* d2 = reinterpret_cast<uint16_t*>(d + a.units);
+        for (int e = 0; e < a.tail; ++e) d2[e] = s2[e];
+    }
+}
+
+// Fewer than kRepGroup destinations: item i is tile round (i / 8) / ndst,
+// destination (i / 8) mod ndst.
 __global__ void __launch_bounds__(kCopyBlock) replicate_kernel(const ReplicateArgs a) {
     const u32x4* __restrict__ src = reinterpret_cast<const u32x4*>(a.dst.ptr[a.from]);
     for (int64_t step = blockIdx.x; step < a.nitems; step += gridDim.x) {
@@ -443,17 +466,22 @@ __global__ void __launch_bounds__(kCopyBlock) replicate_kernel(const ReplicateAr
         const int k = i / kXcds;
         const int t = (k / a.ndst) * kXcds + i % kXcds;
         if (t >= a.ntiles) continue;
-        int j = k % a.ndst;
-        j += j >= a.from;                            // every chunk but the source
-        u32x4* __restrict__ d = reinterpret_cast<u32x4*>(a.dst.ptr[j]);
-        const int64_t g = int64_t(t) * kRepTile + threadIdx.x;
-        if (g < a.units) {
-            __builtin_nontemporal_store(src[g], d + g);
-        } else if (g == a.units && a.tail > 0) {     // one thread copies the partial unit
-            const uint16_t* s2 = reinterpret_cast<const uint16_t*>(src + a.units);
-            uint16_t* d2 = reinterpret_cast<uint16_t*>(d + a.units);
-            for (int e = 0; e < a.tail; ++e) d2[e] = s2[e];
-        }
+        replicate_tile(a, src, t, k % a.ndst);
+    }
+}
+
+// kRepGroup destinations or more: row blockIdx.y holds destinations
+// y*kRepGroup .. y*kRepGroup + kRepGroup - 1 (the last row may be short);
+// item i of a row is tile round (i / 8) / kRepGroup.  `nitems` counts one row.
+__global__ void __launch_bounds__(kCopyBlock) replicate_grouped_kernel(const ReplicateArgs a) {
+    const u32x4* __restrict__ src = reinterpret_cast<const u32x4*>(a.dst.ptr[a.from]);
+    for (int64_t step = blockIdx.x; step < a.nitems; step += gridDim.x) {
+        const int i = int(step);
+        const int k = i >> 3;
+        const int t = ((k >> kRepGroupLog2) << 3) + (i & 7);
+        const int j = int(blockIdx.y) * kRepGroup + (k & (kRepGroup - 1));
+        if (t >= a.ntiles || j >= a.ndst) continue;
+        replicate_tile(a, src, t, j);
     }
 }
 
@@ -921,8 +949,9 @@ fsdp_status load_chunk_table(const Plan& pl, const void* const* chunks, int esiz
 // keeps its work-item count below 2^31, and below FSDP_MAX_WORKGROUPS when
 // that environment variable holds a positive count.
 template <typename Args>
-fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream) {
-    if (ntiles <= 0) return FSDP_OK;
+fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream,
+                   int rows = 1) {
+    if (ntiles <= 0 || rows <= 0) return FSDP_OK;
     fsdp_status st = FSDP_OK;
     const int cus = cu_count(&st);
     if (st != FSDP_OK) return st;
@@ -931,7 +960,7 @@ fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int
         const long long m = std::atoll(env);
         if (m > 0) cap = std::min<int64_t>(cap, m);
     }
-    const dim3 grid(unsigned(std::min<int64_t>(ntiles, cap)));
+    const dim3 grid(unsigned(std::min<int64_t>(ntiles, cap)), unsigned(rows));
     void* kargs[] = {const_cast<Args*>(&args)};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(block), kargs, 0, stream);
     if (e != hipSuccess) return fail(FSDP_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
@@ -1165,12 +1194,15 @@ extern "C" fsdp_status fsdp_ag_pack_push(const fsdp_plan* h, int32_t rank, const
     r.from = rank;
     r.ndst = pl->world - 1;
     const int64_t nt = tiles(r.units + (r.tail > 0), kRepTile);
-    const int64_t items = tiles(nt, kXcds) * kXcds * r.ndst;
+    const bool grouped = r.ndst >= kRepGroup;
+    const int64_t items = tiles(nt, kXcds) * kXcds * (grouped ? kRepGroup : r.ndst);
     if (items > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
     r.ntiles = int32_t(nt);
     r.nitems = int32_t(items);
     if ((st = do_ag_pack(*pl, rank, shards, param_dtype, OneChunk{dst.ptr[rank]}, 1, outs, stream, true)) != FSDP_OK)
         return st;
+    if (grouped)
+        return launch(replicate_grouped_kernel, r, r.nitems, kCopyBlock, stream, int(tiles(r.ndst, kRepGroup)));
     return launch(replicate_kernel, r, r.nitems, kCopyBlock, stream);
 }
 

@@ -204,6 +204,32 @@ def test_ag_pack_push(case):
         plan.close()
 
 
+@pytest.mark.parametrize("W", [15, 16, 17, 18, 33, 34])
+def test_push_destination_rows(W):
+    """The copy half of the push around its row size of 16 destinations:
+    W - 1 = 14 and 15 take one row of every destination, 16 one full row,
+    17 a full row and a row of one, 32 two full rows, 33 two and a row of
+    one; the source rank at either end and inside a row.  Chunks of a few
+    2 KB tiles, whole (align 8) and with a partial 16-byte unit (align 1)."""
+    dims = [(600 * W + 7, 5), (2, 3), (W, 1)]
+    for align in (8, 1):
+        plan = BucketPlan(W, dims, align)
+        oplan = O.make_plan(W, dims, align)
+        S = oplan.chunk
+        for r in sorted({0, 5, W // 2, W - 1}):
+            shards = [random_bits32([W, r, p, 13], O.local_elems(oplan, p, r)).view(np.float32)
+                      for p in range(len(dims))]
+            dsts = _chunks(W, S, "bf16")
+            step(f"ag_pack_push bf16 W={W} rank={r} align={align}")
+            plan.ag_pack_push(r, [to_dev_f32(s_) for s_ in shards], [d.view for d in dsts])
+            torch.cuda.synchronize()
+            want = O.ag_pack(oplan, r, shards, "bf16")
+            for j, d in enumerate(dsts):
+                assert d.guards_intact(), j
+                assert _same(_host(d.view, "bf16"), want), j
+        plan.close()
+
+
 @pytest.mark.parametrize("cap", [1, 7])
 def test_ex_grid_stride(cap, monkeypatch):
     """The element-type and chunk-table forms with every workgroup looping over
