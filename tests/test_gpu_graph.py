@@ -98,8 +98,9 @@ def test_step_replayed_from_a_graph(key):
 
 @pytest.mark.parametrize("W", [4, 8, 48])
 def test_push_replayed_from_a_graph(W):
-    """The push (one kernel below W = 8, a pack and a copy from W = 8 on)
-    captured and replayed: every replay equals the eager push."""
+    """The push (one kernel below W = 8, a pack and a copy from W = 8 on; the
+    copy takes its destinations in grid rows of 16 at W = 48) captured and
+    replayed: every replay equals the eager push."""
     dims = [(3 * W + 1, 64), (W + 3, 1), (5, 8)]
     rank = W // 2
     plan = BucketPlan(W, dims)
