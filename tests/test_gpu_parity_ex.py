@@ -331,6 +331,37 @@ def test_ex_workload_full(key):
     plan.close()
 
 
+@pytest.mark.parametrize("key,align", [(2, 8), (5, 1), (7, 8), (4, 8)])
+def test_push_workload_full(key, align):
+    """The push at full size on the other large buckets: the single-row copy
+    (the 8B block, W = 8) and the copy in rows of 16 (the uneven bucket,
+    W = 48, densely packed so that its chunk ends in a partial 16-byte unit;
+    the 8B block at W = 128; the 405B block, W = 128).  The source rank's
+    chunk is compared with the oracle's pack; every other destination must
+    equal it bit for bit (compared on the device)."""
+    wl = WORKLOADS[key]
+    W = wl.world_size
+    plan = BucketPlan(W, wl.dims, align)
+    oplan = O.make_plan(W, wl.dims, align)
+    S = oplan.chunk
+    P = wl.num_params
+    r = W - 1 if key == 5 else W // 2
+    shards = [random_bits32([key, r, p, 14], O.local_elems(oplan, p, r)).view(np.float32) for p in range(P)]
+    dsts = [torch.empty(S, dtype=torch.bfloat16, device=DEV) for _ in range(W)]
+    for d in dsts:
+        d.view(torch.int16).fill_(-1)
+    step(f"ag_pack_push bf16 full {wl.name} W={W} rank={r} align={align}")
+    plan.ag_pack_push(r, [to_dev_f32(s_) for s_ in shards], dsts)
+    torch.cuda.synchronize()
+    assert np.array_equal(host_u16(dsts[r]), O.ag_pack(oplan, r, shards))
+    src = dsts[r].view(torch.int16)
+    for j in range(W):
+        assert torch.equal(dsts[j].view(torch.int16), src), j
+    del dsts
+    plan.close()
+    torch.cuda.empty_cache()
+
+
 def test_ex_workload_full_chunk_tables():
     """The 70B block (W = 64) at full size through the W-pointer forms the
     benchmark times: unpack pulling W chunks, rs_pack pushing into W chunks,
