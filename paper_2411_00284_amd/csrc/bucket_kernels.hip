@@ -288,7 +288,7 @@ struct PackArgs {
     const float* src[PMAX];
     int64_t off[PMAX + 1];       // off[P] = S
     int64_t valid[PMAX];         // n_{p,rank} * inner_p
-    int32_t tile_start[PMAX];
+    int32_t tile_start[PMAX];    // first tile of parameter p; INT_MAX past the last parameter
     Dst dst;                     // bf16 or fp32 chunks of S elements
     int32_t ndst;                // destinations (1 for OneChunk)
     int32_t nparams;
@@ -385,16 +385,21 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
 }
 
 // Tiles numbered across the bucket; the parameter of a tile comes from the
-// wave-ballot lookup.
+// wave-ballot lookup.  The pack moves few bytes per launch, so its start-up
+// chain is kept short: tile_start holds INT_MAX past the last parameter (no
+// wait for the parameter count before the table load), the grid never exceeds
+// the tile count (the first tile needs no bound check), and a tile's first
+// index comes from the looked-up lane rather than another table load.
 template <int kOut, class Dst>
 __global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs<Dst> a) {
-    const int lane = threadIdx.x & 63;
-    const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
-    for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
+    const int my_start = a.tile_start[threadIdx.x & 63];
+    int64_t step = blockIdx.x;
+    do {
         const int t = int(step);
         const int p = param_of_tile(my_start, t);
-        pack_tile<kOut>(a, p, t - a.tile_start[p]);
-    }
+        pack_tile<kOut>(a, p, t - __builtin_amdgcn_readlane(my_start, p));
+        step += gridDim.x;
+    } while (step < a.ntiles);
 }
 
 // The first half of a wide push: the rank's own chunk, stored through the
@@ -403,13 +408,14 @@ __global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs<Dst>
 // non-temporal stores streamed at little more than half the rate.)
 template <int kOut>
 __global__ void __launch_bounds__(kCopyBlock) push_pack_kernel(const PackArgs<OneChunk> a) {
-    const int lane = threadIdx.x & 63;
-    const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
-    for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
+    const int my_start = a.tile_start[threadIdx.x & 63];
+    int64_t step = blockIdx.x;
+    do {
         const int t = int(step);
         const int p = param_of_tile(my_start, t);
-        pack_tile<kOut, OneChunk, false>(a, p, t - a.tile_start[p]);
-    }
+        pack_tile<kOut, OneChunk, false>(a, p, t - __builtin_amdgcn_readlane(my_start, p));
+        step += gridDim.x;
+    } while (step < a.ntiles);
 }
 
 // The second half of a wide push: chunk `from` copied to the other W - 1
@@ -993,6 +999,7 @@ fsdp_status do_ag_pack(const Plan& pl, int32_t rank, const float* const* shards,
         if (v > 0) ins.push_back(span(shards[p], v * 4));
     }
     a.off[pl.nparams] = pl.chunk;
+    for (int p = pl.nparams; p < PMAX; ++p) a.tile_start[p] = INT32_MAX;   // never a tile's parameter
     a.dst = dst;
     a.ndst = ndst;
     a.nparams = pl.nparams;
