@@ -47,12 +47,10 @@
  *     shared between threads and streams.
  *   - bf16 values are passed as uint16_t bit patterns.
  *   - A launch uses one workgroup per work tile, up to a per-device cap;
- *     past the cap every workgroup loops over several tiles.  The
- *     environment variable FSDP_MAX_WORKGROUPS, when it holds a positive
- *     count, lowers that cap (read at every launch; results do not change).
- *   - The reduction cuts a small shard (fewer than 4 full-size tiles per CU)
- *     into half-size tiles; FSDP_REDUCE_HALF_TILES=0 or 1 forces full- or
- *     half-size tiles (read at every launch; results do not change).
+ *     past the cap every workgroup loops over several tiles.  The reduction
+ *     cuts a small shard (fewer than 4 full-size tiles per CU) into
+ *     half-size tiles.  A plan made by fsdp_bucket_plan_ex may lower the cap
+ *     or force the tile size; results never depend on either.
  */
 #ifndef FSDP_BUCKET_H
 #define FSDP_BUCKET_H
@@ -111,6 +109,29 @@ typedef struct fsdp_plan fsdp_plan;
 fsdp_status fsdp_bucket_plan(int32_t world_size, int32_t num_params,
                              const int64_t* dim0, const int64_t* inner,
                              int32_t align_elems, fsdp_plan** out);
+
+/* Launch options of a plan (fsdp_bucket_plan_ex).  They change how the work
+ * is cut into workgroups, never a result bit. */
+enum {
+    FSDP_REDUCE_TILES_AUTO = 0,   /* half-size tiles below 4 full-size tiles per CU */
+    FSDP_REDUCE_TILES_FULL = 1,   /* always 256-thread tiles */
+    FSDP_REDUCE_TILES_HALF = 2    /* always 128-thread tiles */
+};
+typedef struct fsdp_plan_options {
+    int64_t max_workgroups;   /* > 0: no launch of the plan has a larger grid
+                                 (workgroups loop over tiles); 0: the default */
+    int32_t reduce_tiles;     /* FSDP_REDUCE_TILES_*; 0 is the default */
+    int32_t reserved;         /* must be 0 */
+} fsdp_plan_options;
+
+/* fsdp_bucket_plan with launch options (NULL = all defaults), fixed for the
+ * plan's lifetime.  Errors: those of fsdp_bucket_plan, and FSDP_ERR_INVALID
+ * for a negative max_workgroups, an unknown reduce_tiles or a non-zero
+ * reserved field.  Makes no HIP call. */
+fsdp_status fsdp_bucket_plan_ex(int32_t world_size, int32_t num_params,
+                                const int64_t* dim0, const int64_t* inner,
+                                int32_t align_elems, const fsdp_plan_options* options,
+                                fsdp_plan** out);
 
 /* Release a plan (NULL is ignored). */
 void fsdp_plan_free(fsdp_plan* plan);

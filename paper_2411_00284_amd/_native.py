@@ -25,6 +25,9 @@ SIGNATURES = {
     "fsdp_bucket_plan": (c_status, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
                                     ctypes.POINTER(ctypes.c_int64), ctypes.c_int32,
                                     ctypes.POINTER(ctypes.c_void_p)]),
+    "fsdp_bucket_plan_ex": (c_status, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
+                                       ctypes.POINTER(ctypes.c_int64), ctypes.c_int32, ctypes.c_void_p,
+                                       ctypes.POINTER(ctypes.c_void_p)]),
     "fsdp_plan_free": (None, [c_plan_p]),
     "fsdp_plan_chunk_elems": (ctypes.c_int64, [c_plan_p]),
     "fsdp_plan_world_size": (ctypes.c_int32, [c_plan_p]),
@@ -54,6 +57,13 @@ SIGNATURES = {
                                   ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
 }
 
+class PlanOptions(ctypes.Structure):
+    """struct fsdp_plan_options."""
+    _fields_ = [("max_workgroups", ctypes.c_int64), ("reduce_tiles", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+REDUCE_TILES = {"auto": 0, "full": 1, "half": 2}
 MAX_PARAMS = 64
 MAX_CHUNKS = 128
 DTYPE_BF16 = 0

@@ -124,18 +124,25 @@ class BucketPlan:
     """A bucket of parameters sharded on dim 0 over ``world_size`` ranks.
 
     ``shapes`` are the full parameter shapes (dim 0 is sharded, the trailing
-    dims are flattened into ``inner``), in bucket order.
+    dims are flattened into ``inner``), in bucket order.  ``max_workgroups``
+    (> 0) caps every launch's grid and ``reduce_tiles`` ("auto", "full" or
+    "half") fixes the reduction's tile size; neither changes a result.
     """
 
-    def __init__(self, world_size: int, shapes: Sequence, align: int = 8):
+    def __init__(self, world_size: int, shapes: Sequence, align: int = 8, max_workgroups: int = 0,
+                 reduce_tiles: str = "auto"):
         self._lib = _native.load()
         dims = [_rows_inner(s) for s in shapes]
         n = len(dims)
         rows = (ctypes.c_int64 * max(n, 1))(*[d[0] for d in dims])
         inner = (ctypes.c_int64 * max(n, 1))(*[d[1] for d in dims])
+        if reduce_tiles not in _native.REDUCE_TILES:
+            raise ValueError("reduce_tiles must be 'auto', 'full' or 'half'")
+        opts = _native.PlanOptions(int(max_workgroups), _native.REDUCE_TILES[reduce_tiles], 0)
         h = ctypes.c_void_p()
-        _check(self._lib.fsdp_bucket_plan(int(world_size), n, rows, inner, int(align), ctypes.byref(h)),
-               "fsdp_bucket_plan")
+        _check(self._lib.fsdp_bucket_plan_ex(int(world_size), n, rows, inner, int(align), ctypes.byref(opts),
+                                             ctypes.byref(h)),
+               "fsdp_bucket_plan_ex")
         self._h = h
         self.world_size = int(world_size)
         self.num_params = n

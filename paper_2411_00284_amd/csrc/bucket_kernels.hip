@@ -18,8 +18,8 @@
 // an exchange fused with the copy: the chunks of the peers).
 //
 // Numerics (SimpleFSDP sections 3.2.1 and 4):
-//   * fp32 -> bf16 is IEEE round-half-to-even on the 16 dropped bits; NaN
-//     gives (bits >> 16) | 0x0040;
+//   * fp32 -> bf16 is IEEE round-half-to-even on the 16 dropped bits (the
+//     hardware conversion); NaN gives (bits >> 16) | 0x0040;
 //   * bf16 -> fp32 is exact (append 16 zero bits); fp32 copies are bit copies;
 //   * the average is an fp32 sum over source ranks in order 0..W-1, starting
 //     from the rank-0 value, then one IEEE division by W.  The library is
@@ -63,15 +63,19 @@ constexpr int kBlocksPerCU = FSDP_BLOCKS_PER_CU;  // workgroups per CU in the gr
 
 // ------------------------------------------------------------------ device helpers
 
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
+// fp32 -> bf16 with gfx950's packed conversion (v_cvt_pk_bf16_f32): IEEE
+// round-half-to-even on the 16 dropped bits under the default rounding mode,
+// subnormals kept, overflow to infinity; a NaN keeps its sign and top payload
+// bits and gets the quiet bit, (bits >> 16) | 0x0040.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t bf16x2_bits(float lo, float hi) {
-    return bf16_bits(lo) | (bf16_bits(hi) << 16);
+    const f32x2_t f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
+
+__device__ __forceinline__ uint32_t bf16_bits(float f) { return bf16x2_bits(f, 0.f) & 0xffffu; }
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -301,6 +305,7 @@ template <int kOut>
 __device__ __forceinline__ uint32_t cast1(float f) { return kOut == kF16 ? f16_bits(f) : bf16_bits(f); }
 template <int kOut>
 __device__ __forceinline__ uint2 cast4(float4 a) {
+    if constexpr (kOut == kBF16) return make_uint2(bf16x2_bits(a.x, a.y), bf16x2_bits(a.z, a.w));
     return make_uint2(cast1<kOut>(a.x) | (cast1<kOut>(a.y) << 16), cast1<kOut>(a.z) | (cast1<kOut>(a.w) << 16));
 }
 
@@ -333,7 +338,7 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
             uint4 y[kPackSteps];
 #pragma unroll
             for (int u = 0; u < kPackSteps; ++u) {
-                const float* s8 = src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 8;
+                const float* s8 = src + lo + (int64_t(u) * kPackBlock + threadIdx.x) * 8;
                 const uint2 c0 = cast4<kOut>(ld16f(s8));
                 const uint2 c1 = cast4<kOut>(ld16f(s8 + 4));
                 y[u] = make_uint4(c0.x, c0.y, c1.x, c1.y);
@@ -341,7 +346,7 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
             for (int j = 0; j < ndst; ++j) {
                 Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
 #pragma unroll
-                for (int u = 0; u < kPackSteps; ++u) st16<kNt>(dst + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 8, y[u]);
+                for (int u = 0; u < kPackSteps; ++u) st16<kNt>(dst + lo + (int64_t(u) * kPackBlock + threadIdx.x) * 8, y[u]);
             }
             return;
         }
@@ -349,12 +354,12 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
     if (vec && hi - lo == kPackTile && lo + kPackTile <= valid) {
         float4 x[kSub];
 #pragma unroll
-        for (int u = 0; u < kSub; ++u) x[u] = ld16f(src + lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4);
+        for (int u = 0; u < kSub; ++u) x[u] = ld16f(src + lo + (int64_t(u) * kPackBlock + threadIdx.x) * 4);
         for (int j = 0; j < ndst; ++j) {
             Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
 #pragma unroll
             for (int u = 0; u < kSub; ++u) {
-                const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
+                const int64_t g = lo + (int64_t(u) * kPackBlock + threadIdx.x) * 4;
                 if (kCast) st8<kNt>(dst + g, cast4<kOut>(x[u]));
                 else st16f<kNt>(reinterpret_cast<float*>(dst + g), x[u]);
             }
@@ -362,7 +367,7 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
         return;
     }
     for (int u = 0; u < kSub; ++u) {
-        const int64_t g = lo + (int64_t(u) * kCopyBlock + threadIdx.x) * 4;
+        const int64_t g = lo + (int64_t(u) * kPackBlock + threadIdx.x) * 4;
         if (g >= hi) break;
         if (vec && g + 4 <= hi && (g + 4 <= valid || g >= valid)) {
             const float4 x = g < valid ? ld16f(src + g) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -391,7 +396,7 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
 // the tile count (the first tile needs no bound check), and a tile's first
 // index comes from the looked-up lane rather than another table load.
 template <int kOut, class Dst>
-__global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs<Dst> a) {
+__global__ void __launch_bounds__(kPackBlock) ag_pack_kernel(const PackArgs<Dst> a) {
     const int my_start = a.tile_start[threadIdx.x & 63];
     int64_t step = blockIdx.x;
     do {
@@ -407,7 +412,7 @@ __global__ void __launch_bounds__(kCopyBlock) ag_pack_kernel(const PackArgs<Dst>
 // the MALL.  (Read back at once by many workgroups, a chunk just written with
 // non-temporal stores streamed at little more than half the rate.)
 template <int kOut>
-__global__ void __launch_bounds__(kCopyBlock) push_pack_kernel(const PackArgs<OneChunk> a) {
+__global__ void __launch_bounds__(kPackBlock) push_pack_kernel(const PackArgs<OneChunk> a) {
     const int my_start = a.tile_start[threadIdx.x & 63];
     int64_t step = blockIdx.x;
     do {
@@ -896,26 +901,42 @@ struct Span {
     uintptr_t lo, hi;   // [lo, hi) bytes
 };
 
-Span span(const void* p, int64_t bytes) { return {uintptr_t(p), uintptr_t(p) + uintptr_t(bytes)}; }
+// The byte spans of one call's inputs or outputs, on the stack: at most one
+// per parameter or one per chunk of a table, so the hot calls allocate
+// nothing on the host either.
+constexpr int kMaxSpans = (PMAX > kMaxChunks ? PMAX : kMaxChunks) + 1;
+struct Spans {
+    Span s[kMaxSpans];
+    int n = 0;
+    void add(const void* p, int64_t bytes) {
+        if (n < kMaxSpans) s[n++] = {uintptr_t(p), uintptr_t(p) + uintptr_t(bytes)};
+    }
+};
 
 // Outputs must be pairwise disjoint and disjoint from every input.
-fsdp_status check_overlap(std::vector<Span> outs, const std::vector<Span>& ins) {
-    std::sort(outs.begin(), outs.end(), [](const Span& a, const Span& b) { return a.lo < b.lo; });
-    for (size_t k = 1; k < outs.size(); ++k)
-        if (outs[k].lo < outs[k - 1].hi) return fail(FSDP_ERR_OVERLAP, "two outputs overlap");
-    for (const Span& in : ins) {
+fsdp_status check_overlap(const Spans& out_spans, const Spans& ins) {
+    Spans outs = out_spans;
+    Span* const b = outs.s;
+    Span* const e = outs.s + outs.n;
+    std::sort(b, e, [](const Span& x, const Span& y) { return x.lo < y.lo; });
+    for (int k = 1; k < outs.n; ++k)
+        if (b[k].lo < b[k - 1].hi) return fail(FSDP_ERR_OVERLAP, "two outputs overlap");
+    for (int k = 0; k < ins.n; ++k) {
+        const Span& in = ins.s[k];
         // first output ending after in.lo
-        auto it = std::upper_bound(outs.begin(), outs.end(), in.lo,
-                                   [](uintptr_t v, const Span& s) { return v < s.hi; });
-        if (it != outs.end() && it->lo < in.hi) return fail(FSDP_ERR_OVERLAP, "an output overlaps an input");
+        const Span* it = std::upper_bound(b, e, in.lo, [](uintptr_t v, const Span& x) { return v < x.hi; });
+        if (it != e && it->lo < in.hi) return fail(FSDP_ERR_OVERLAP, "an output overlaps an input");
     }
     return FSDP_OK;
 }
 
-fsdp_status check_bucket_ptr(const void* ptr, int64_t elems, const std::string& name) {
-    if (elems > 0 && ptr == nullptr) return fail(FSDP_ERR_INVALID, name + " is NULL");
-    if ((reinterpret_cast<uintptr_t>(ptr) & 15) != 0) return fail(FSDP_ERR_ALIGN, name + " is not 16-byte aligned");
-    return FSDP_OK;
+// `index` >= 0 names element `index` of the array `name`.
+fsdp_status check_bucket_ptr(const void* ptr, int64_t elems, const char* name, int index = -1) {
+    const bool null = elems > 0 && ptr == nullptr;
+    if (!null && (reinterpret_cast<uintptr_t>(ptr) & 15) == 0) return FSDP_OK;
+    const std::string what = index < 0 ? std::string(name) : std::string(name) + "[" + std::to_string(index) + "]";
+    if (null) return fail(FSDP_ERR_INVALID, what + " is NULL");
+    return fail(FSDP_ERR_ALIGN, what + " is not 16-byte aligned");
 }
 
 fsdp_status check_param_ptr(const void* ptr, int64_t elems, int elem_bytes, int p, const char* what) {
@@ -938,34 +959,31 @@ int elem_bytes(fsdp_dtype t) { return t == FSDP_DTYPE_F32 ? 4 : 2; }
 // A host array of W chunk pointers, each 16-byte aligned and non-NULL when
 // chunks have elements.
 fsdp_status load_chunk_table(const Plan& pl, const void* const* chunks, int esize, TableChunks* out,
-                             std::vector<Span>* spans) {
+                             Spans* spans) {
     if (chunks == nullptr) return fail(FSDP_ERR_INVALID, "chunks is NULL");
     if (pl.world > kMaxChunks) return fail(FSDP_ERR_TOO_MANY, "world size exceeds FSDP_MAX_CHUNKS");
     fsdp_status st;
     for (int i = 0; i < pl.world; ++i) {
-        if ((st = check_bucket_ptr(chunks[i], pl.chunk, "chunks[" + std::to_string(i) + "]")) != FSDP_OK) return st;
+        if ((st = check_bucket_ptr(chunks[i], pl.chunk, "chunks", i)) != FSDP_OK) return st;
         out->ptr[i] = static_cast<char*>(const_cast<void*>(chunks[i]));
-        if (pl.chunk > 0) spans->push_back(span(chunks[i], pl.chunk * esize));
+        if (pl.chunk > 0) spans->add(chunks[i], pl.chunk * esize);
     }
     return FSDP_OK;
 }
 
 // One launch of `kernel` over `ntiles` work tiles, one tile per workgroup up
 // to kBlocksPerCU workgroups per CU (grid-stride beyond that).  The grid also
-// keeps its work-item count below 2^31, and below FSDP_MAX_WORKGROUPS when
-// that environment variable holds a positive count.
+// keeps its work-item count below 2^31, and below the plan's max_workgroups
+// when that is positive.
 template <typename Args>
-fsdp_status launch(void (*kernel)(const Args), const Args& args, int ntiles, int block, hipStream_t stream,
-                   int rows = 1) {
+fsdp_status launch(const Plan& pl, void (*kernel)(const Args), const Args& args, int ntiles, int block,
+                   hipStream_t stream, int rows = 1) {
     if (ntiles <= 0 || rows <= 0) return FSDP_OK;
     fsdp_status st = FSDP_OK;
     const int cus = cu_count(&st);
     if (st != FSDP_OK) return st;
     int64_t cap = std::min<int64_t>(int64_t(cus) * kBlocksPerCU, (int64_t(1) << 31) / block);
-    if (const char* env = std::getenv("FSDP_MAX_WORKGROUPS")) {
-        const long long m = std::atoll(env);
-        if (m > 0) cap = std::min<int64_t>(cap, m);
-    }
+    if (pl.max_workgroups > 0) cap = std::min<int64_t>(cap, pl.max_workgroups);
     const dim3 grid(unsigned(std::min<int64_t>(ntiles, cap)), unsigned(rows));
     void* kargs[] = {const_cast<Args*>(&args)};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(block), kargs, 0, stream);
@@ -981,12 +999,12 @@ int64_t tiles(int64_t n, int64_t tile) { return (n + tile - 1) / tile; }
 // (TableChunks); `outs` holds their byte spans for the overlap check.
 template <class Dst>
 fsdp_status do_ag_pack(const Plan& pl, int32_t rank, const float* const* shards, fsdp_dtype wire, const Dst& dst,
-                       int ndst, const std::vector<Span>& outs, hipStream_t stream, bool cached = false) {
+                       int ndst, const Spans& outs, hipStream_t stream, bool cached = false) {
     fsdp_status st;
     if (rank < 0 || rank >= pl.world) return fail(FSDP_ERR_INVALID, "rank out of range");
     if (shards == nullptr) return fail(FSDP_ERR_INVALID, "shards is NULL");
     PackArgs<Dst> a{};
-    std::vector<Span> ins;
+    Spans ins;
     int64_t nt = 0;   // at most the planner's checked pack tile count
     for (int p = 0; p < pl.nparams; ++p) {
         const int64_t v = pl.local_elems(p, rank);
@@ -996,7 +1014,7 @@ fsdp_status do_ag_pack(const Plan& pl, int32_t rank, const float* const* shards,
         a.valid[p] = v;
         a.tile_start[p] = int32_t(nt);
         nt += tiles(pl.off[p + 1] - pl.off[p], kPackTile);
-        if (v > 0) ins.push_back(span(shards[p], v * 4));
+        if (v > 0) ins.add(shards[p], v * 4);
     }
     a.off[pl.nparams] = pl.chunk;
     for (int p = pl.nparams; p < PMAX; ++p) a.tile_start[p] = INT32_MAX;   // never a tile's parameter
@@ -1008,14 +1026,14 @@ fsdp_status do_ag_pack(const Plan& pl, int32_t rank, const float* const* shards,
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
     if constexpr (std::is_same<Dst, OneChunk>::value) {
         if (cached) {
-            if (wire == FSDP_DTYPE_BF16) return launch(push_pack_kernel<kBF16>, a, a.ntiles, kCopyBlock, stream);
-            if (wire == FSDP_DTYPE_F16) return launch(push_pack_kernel<kF16>, a, a.ntiles, kCopyBlock, stream);
-            return launch(push_pack_kernel<kF32>, a, a.ntiles, kCopyBlock, stream);
+            if (wire == FSDP_DTYPE_BF16) return launch(pl, push_pack_kernel<kBF16>, a, a.ntiles, kPackBlock, stream);
+            if (wire == FSDP_DTYPE_F16) return launch(pl, push_pack_kernel<kF16>, a, a.ntiles, kPackBlock, stream);
+            return launch(pl, push_pack_kernel<kF32>, a, a.ntiles, kPackBlock, stream);
         }
     }
-    if (wire == FSDP_DTYPE_BF16) return launch(ag_pack_kernel<kBF16, Dst>, a, a.ntiles, kCopyBlock, stream);
-    if (wire == FSDP_DTYPE_F16) return launch(ag_pack_kernel<kF16, Dst>, a, a.ntiles, kCopyBlock, stream);
-    return launch(ag_pack_kernel<kF32, Dst>, a, a.ntiles, kCopyBlock, stream);
+    if (wire == FSDP_DTYPE_BF16) return launch(pl, ag_pack_kernel<kBF16, Dst>, a, a.ntiles, kPackBlock, stream);
+    if (wire == FSDP_DTYPE_F16) return launch(pl, ag_pack_kernel<kF16, Dst>, a, a.ntiles, kPackBlock, stream);
+    return launch(pl, ag_pack_kernel<kF32, Dst>, a, a.ntiles, kPackBlock, stream);
 }
 
 fsdp_status do_ag_pack_one(const fsdp_plan* h, int32_t rank, const float* const* shards, fsdp_dtype wire,
@@ -1026,20 +1044,20 @@ fsdp_status do_ag_pack_one(const fsdp_plan* h, int32_t rank, const float* const*
     if (!pl) return st;
     if (!known_dtype(wire)) return fail(FSDP_ERR_INVALID, "unknown dtype");
     if ((st = check_bucket_ptr(send_chunk, pl->chunk, "send_chunk")) != FSDP_OK) return st;
-    std::vector<Span> outs;
-    if (pl->chunk > 0) outs.push_back(span(send_chunk, pl->chunk * elem_bytes(wire)));
+    Spans outs;
+    if (pl->chunk > 0) outs.add(send_chunk, pl->chunk * elem_bytes(wire));
     return do_ag_pack(*pl, rank, shards, wire, OneChunk{static_cast<char*>(send_chunk)}, 1, outs, stream);
 }
 
 // ---- ag_unpack: u = 2-byte units per element
 
 template <class Chunks>
-fsdp_status do_ag_unpack(const Plan& pl, const Chunks& src, const std::vector<Span>& ins, int u,
+fsdp_status do_ag_unpack(const Plan& pl, const Chunks& src, const Spans& ins, int u,
                          void* const* params, hipStream_t stream) {
     fsdp_status st;
     if (params == nullptr) return fail(FSDP_ERR_INVALID, "params is NULL");
     UnpackArgs<Chunks> a{};
-    std::vector<Span> outs;
+    Spans outs;
     int64_t nt = 0;
     for (int p = 0; p < pl.nparams; ++p) {
         const int64_t e = pl.elems[p];
@@ -1054,13 +1072,13 @@ fsdp_status do_ag_unpack(const Plan& pl, const Chunks& src, const std::vector<Sp
         a.tile_start[p] = int32_t(nt);
         nt += int64_t(pl.world) * a.tiles_per_seg[p];
         if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
-        if (e > 0) outs.push_back(span(params[p], e * 2 * u));
+        if (e > 0) outs.add(params[p], e * 2 * u);
     }
     a.src = src;
     a.nparams = pl.nparams;
     a.ntiles = int32_t(nt);
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    return launch(ag_unpack_kernel<Chunks>, a, a.ntiles, kCopyBlock, stream);
+    return launch(pl, ag_unpack_kernel<Chunks>, a, a.ntiles, kCopyBlock, stream);
 }
 
 // ---- rs_pack: gradient elements of `gsize` bytes; kWiden (kBF16 / kF16) casts
@@ -1068,12 +1086,12 @@ fsdp_status do_ag_unpack(const Plan& pl, const Chunks& src, const std::vector<Sp
 
 template <class Chunks, int kWiden>
 fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, const Chunks& dst,
-                       const std::vector<Span>& outs, hipStream_t stream) {
+                       const Spans& outs, hipStream_t stream) {
     fsdp_status st;
     if (grads == nullptr) return fail(FSDP_ERR_INVALID, "grads is NULL");
     const int u = kWiden != kF32 ? 1 : gsize / 2;     // kernel units per element
     RsPackArgs<Chunks> a{};
-    std::vector<Span> ins;
+    Spans ins;
     int64_t nt = 0;
     for (int p = 0; p < pl.nparams; ++p) {
         const int64_t e = pl.elems[p];
@@ -1088,7 +1106,7 @@ fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, cons
         a.tile_start[p] = int32_t(nt);                  // rescaled below for the parameter-major order
         nt += tps;
         if (nt * pl.world > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
-        if (e > 0) ins.push_back(span(grads[p], e * gsize));
+        if (e > 0) ins.add(grads[p], e * gsize);
     }
     a.dest_major = pl.world > kDestMajorW;
     if (!a.dest_major)
@@ -1099,22 +1117,22 @@ fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, cons
     a.tiles_per_dest = int32_t(nt);
     a.ntiles = int32_t(nt * pl.world);
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    return launch(rs_pack_kernel<Chunks, kWiden>, a, a.ntiles, kCopyBlock, stream);
+    return launch(pl, rs_pack_kernel<Chunks, kWiden>, a, a.ntiles, kCopyBlock, stream);
 }
 
 // ---- rs_reduce: received elements of type T
 
 template <class Chunks, typename T>
-fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const std::vector<Span>& ins,
+fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const Spans& ins,
                          float* const* grad_shards, hipStream_t stream) {
     fsdp_status st = FSDP_OK;
     if (grad_shards == nullptr) return fail(FSDP_ERR_INVALID, "grad_shards is NULL");
-    std::vector<Span> outs;
+    Spans outs;
     int64_t full_tiles = 0;
     for (int p = 0; p < pl.nparams; ++p) {
         const int64_t v = pl.local_elems(p, rank);
         if ((st = check_param_ptr(grad_shards[p], v, 4, p, "grad_shards")) != FSDP_OK) return st;
-        if (v > 0) outs.push_back(span(grad_shards[p], v * 4));
+        if (v > 0) outs.add(grad_shards[p], v * 4);
         full_tiles += tiles(v, kReduceTile);
     }
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
@@ -1126,21 +1144,22 @@ fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const 
     const int cus = cu_count(&st);
     if (st != FSDP_OK) return st;
     bool small = full_tiles < int64_t(kSmallShardTilesPerCU) * cus;
-    if (const char* env = std::getenv("FSDP_REDUCE_HALF_TILES")) {   // "0" or "1" forces the choice
-        if (env[0] == '0') small = false;
-        if (env[0] == '1') small = true;
-    }
+    if (pl.reduce_tiles == FSDP_REDUCE_TILES_FULL) small = false;
+    if (pl.reduce_tiles == FSDP_REDUCE_TILES_HALF) small = true;
     const int64_t tile = small ? kReduceTile / 2 : kReduceTile;
     // Tiles of the parameters with the fewest tiles are numbered (and so
     // dispatched) first: a ragged last tile sums its W sources in a longer
     // dependent chain, which then overlaps the bulk instead of trailing it.
-    std::vector<int> order(pl.nparams);
-    std::vector<int64_t> nts(pl.nparams);
+    // (A stable insertion sort of at most FSDP_MAX_PARAMS entries: equal
+    // counts keep the bucket order, and nothing is allocated.)
+    int order[PMAX];
+    int64_t nts[PMAX];
     for (int p = 0; p < pl.nparams; ++p) {
-        order[p] = p;
         nts[p] = tiles(pl.local_elems(p, rank), tile);
+        int q = p;
+        for (; q > 0 && nts[order[q - 1]] > nts[p]; --q) order[q] = order[q - 1];
+        order[q] = p;
     }
-    std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return nts[x] < nts[y]; });
     ReduceArgs<Chunks> a{};
     int64_t nt = 0;
     for (int q = 0; q < pl.nparams; ++q) {
@@ -1156,8 +1175,8 @@ fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const 
     a.world = pl.world;
     a.nparams = pl.nparams;
     a.ntiles = int32_t(nt);
-    if (small) return launch(rs_reduce_kernel<Chunks, T, kReduceBlock / 2>, a, a.ntiles, kReduceBlock / 2, stream);
-    return launch(rs_reduce_kernel<Chunks, T, kReduceBlock>, a, a.ntiles, kReduceBlock, stream);
+    if (small) return launch(pl, rs_reduce_kernel<Chunks, T, kReduceBlock / 2>, a, a.ntiles, kReduceBlock / 2, stream);
+    return launch(pl, rs_reduce_kernel<Chunks, T, kReduceBlock>, a, a.ntiles, kReduceBlock, stream);
 }
 
 }  // namespace
@@ -1185,7 +1204,7 @@ extern "C" fsdp_status fsdp_ag_pack_push(const fsdp_plan* h, int32_t rank, const
     if (rank < 0 || rank >= pl->world) return fail(FSDP_ERR_INVALID, "rank out of range");
     const int esize = elem_bytes(param_dtype);
     TableChunks dst{};
-    std::vector<Span> outs;
+    Spans outs;
     if ((st = load_chunk_table(*pl, const_cast<const void* const*>(chunks), esize, &dst, &outs)) != FSDP_OK)
         return st;
     if (pl->world < kReplicateMinW || pl->chunk == 0)
@@ -1209,8 +1228,8 @@ extern "C" fsdp_status fsdp_ag_pack_push(const fsdp_plan* h, int32_t rank, const
     if ((st = do_ag_pack(*pl, rank, shards, param_dtype, OneChunk{dst.ptr[rank]}, 1, outs, stream, true)) != FSDP_OK)
         return st;
     if (grouped)
-        return launch(replicate_grouped_kernel, r, r.nitems, kCopyBlock, stream, int(tiles(r.ndst, kRepGroup)));
-    return launch(replicate_kernel, r, r.nitems, kCopyBlock, stream);
+        return launch(*pl, replicate_grouped_kernel, r, r.nitems, kCopyBlock, stream, int(tiles(r.ndst, kRepGroup)));
+    return launch(*pl, replicate_kernel, r, r.nitems, kCopyBlock, stream);
 }
 
 extern "C" fsdp_status fsdp_ag_unpack(const fsdp_plan* h, const uint16_t* gathered, uint16_t* const* params,
@@ -1221,8 +1240,8 @@ extern "C" fsdp_status fsdp_ag_unpack(const fsdp_plan* h, const uint16_t* gather
     if (!pl) return st;
     const int64_t total = int64_t(pl->world) * pl->chunk;
     if ((st = check_bucket_ptr(gathered, total, "gathered")) != FSDP_OK) return st;
-    std::vector<Span> ins;
-    if (total > 0) ins.push_back(span(gathered, total * 2));
+    Spans ins;
+    if (total > 0) ins.add(gathered, total * 2);
     const ContigChunks src{reinterpret_cast<char*>(const_cast<uint16_t*>(gathered)), pl->chunk * 2};
     return do_ag_unpack(*pl, src, ins, 1, reinterpret_cast<void* const*>(params), stream);
 }
@@ -1236,7 +1255,7 @@ extern "C" fsdp_status fsdp_ag_unpack_ex(const fsdp_plan* h, fsdp_dtype param_dt
     if (!known_dtype(param_dtype)) return fail(FSDP_ERR_INVALID, "unknown dtype");
     const int esize = elem_bytes(param_dtype);
     TableChunks src{};
-    std::vector<Span> ins;
+    Spans ins;
     if ((st = load_chunk_table(*pl, chunks, esize, &src, &ins)) != FSDP_OK) return st;
     return do_ag_unpack(*pl, src, ins, esize / 2, params, stream);
 }
@@ -1249,8 +1268,8 @@ extern "C" fsdp_status fsdp_rs_pack(const fsdp_plan* h, const uint16_t* const* g
     if (!pl) return st;
     const int64_t total = int64_t(pl->world) * pl->chunk;
     if ((st = check_bucket_ptr(send_buf, total, "send_buf")) != FSDP_OK) return st;
-    std::vector<Span> outs;
-    if (total > 0) outs.push_back(span(send_buf, total * 2));
+    Spans outs;
+    if (total > 0) outs.add(send_buf, total * 2);
     const ContigChunks dst{reinterpret_cast<char*>(send_buf), pl->chunk * 2};
     return do_rs_pack<ContigChunks, kF32>(*pl, reinterpret_cast<const void* const*>(grads), 2, dst, outs, stream);
 }
@@ -1267,7 +1286,7 @@ extern "C" fsdp_status fsdp_rs_pack_ex(const fsdp_plan* h, fsdp_dtype grad_dtype
     if (reduce_dtype != grad_dtype && reduce_dtype != FSDP_DTYPE_F32)
         return fail(FSDP_ERR_INVALID, "the wire must have the gradients' type or be fp32");
     TableChunks dst{};
-    std::vector<Span> outs;
+    Spans outs;
     if ((st = load_chunk_table(*pl, chunks, elem_bytes(reduce_dtype), &dst, &outs)) != FSDP_OK) return st;
     if (grad_dtype == FSDP_DTYPE_BF16 && reduce_dtype == FSDP_DTYPE_F32)
         return do_rs_pack<TableChunks, kBF16>(*pl, grads, 2, dst, outs, stream);
@@ -1285,8 +1304,8 @@ extern "C" fsdp_status fsdp_rs_reduce(const fsdp_plan* h, int32_t rank, const ui
     if (rank < 0 || rank >= pl->world) return fail(FSDP_ERR_INVALID, "rank out of range");
     const int64_t total = int64_t(pl->world) * pl->chunk;
     if ((st = check_bucket_ptr(recv, total, "recv")) != FSDP_OK) return st;
-    std::vector<Span> ins;
-    if (total > 0) ins.push_back(span(recv, total * 2));
+    Spans ins;
+    if (total > 0) ins.add(recv, total * 2);
     const ContigChunks src{reinterpret_cast<char*>(const_cast<uint16_t*>(recv)), pl->chunk * 2};
     return do_rs_reduce<ContigChunks, uint16_t>(*pl, rank, src, ins, grad_shards, stream);
 }
@@ -1300,7 +1319,7 @@ extern "C" fsdp_status fsdp_rs_reduce_ex(const fsdp_plan* h, int32_t rank, fsdp_
     if (!known_dtype(reduce_dtype)) return fail(FSDP_ERR_INVALID, "unknown dtype");
     if (rank < 0 || rank >= pl->world) return fail(FSDP_ERR_INVALID, "rank out of range");
     TableChunks src{};
-    std::vector<Span> ins;
+    Spans ins;
     if ((st = load_chunk_table(*pl, chunks, elem_bytes(reduce_dtype), &src, &ins)) != FSDP_OK) return st;
     if (reduce_dtype == FSDP_DTYPE_F32) return do_rs_reduce<TableChunks, float>(*pl, rank, src, ins, grad_shards, stream);
     if (reduce_dtype == FSDP_DTYPE_F16)

@@ -57,9 +57,23 @@ using namespace fsdp;
 extern "C" fsdp_status fsdp_bucket_plan(int32_t world_size, int32_t num_params,
                                         const int64_t* dim0, const int64_t* inner,
                                         int32_t align_elems, fsdp_plan** out) {
+    return fsdp_bucket_plan_ex(world_size, num_params, dim0, inner, align_elems, nullptr, out);
+}
+
+extern "C" fsdp_status fsdp_bucket_plan_ex(int32_t world_size, int32_t num_params,
+                                           const int64_t* dim0, const int64_t* inner,
+                                           int32_t align_elems, const fsdp_plan_options* options,
+                                           fsdp_plan** out) {
     clear_error();
     if (out == nullptr) return fail(FSDP_ERR_INVALID, "out is NULL");
     *out = nullptr;
+    if (options != nullptr) {
+        if (options->max_workgroups < 0) return fail(FSDP_ERR_INVALID, "max_workgroups must be >= 0");
+        if (options->reduce_tiles != FSDP_REDUCE_TILES_AUTO && options->reduce_tiles != FSDP_REDUCE_TILES_FULL &&
+            options->reduce_tiles != FSDP_REDUCE_TILES_HALF)
+            return fail(FSDP_ERR_INVALID, "unknown reduce_tiles");
+        if (options->reserved != 0) return fail(FSDP_ERR_INVALID, "reserved must be 0");
+    }
     if (world_size < 1) return fail(FSDP_ERR_INVALID, "world_size must be >= 1");
     if (num_params < 1) return fail(FSDP_ERR_INVALID, "num_params must be >= 1");
     if (num_params > FSDP_MAX_PARAMS)
@@ -98,6 +112,10 @@ extern "C" fsdp_status fsdp_bucket_plan(int32_t world_size, int32_t num_params,
         return fail(FSDP_ERR_OVERFLOW, "W*S too large");
     pl.chunk = S;
     pl.off.push_back(S);
+    if (options != nullptr) {
+        pl.max_workgroups = options->max_workgroups;
+        pl.reduce_tiles = options->reduce_tiles;
+    }
 
     // Work tiles of each kernel must be countable in 31 bits.
     int64_t t_pack = 0, t_copy = 0, t_reduce = 0;

@@ -9,11 +9,13 @@
 
 namespace fsdp {
 
-// Work tiles.  The copy kernels (ag_pack, ag_unpack, rs_pack) run
-// kCopyBlock threads that move 8 elements (16 bytes of bf16) per thread and
-// step, kCopySteps steps per tile (kPackSteps for ag_pack); the reduction
-// runs kReduceBlock threads that each own kReduceSteps groups of 8 outputs.  One tile per workgroup
-// (small tiles, many workgroups) measured fastest for these HBM streams.
+// Work tiles.  The copy kernels (ag_unpack, rs_pack) run kCopyBlock threads
+// that move 8 elements (16 bytes of bf16) per thread and step, kCopySteps
+// steps per tile; ag_pack runs kPackBlock threads that cast 8 elements per
+// thread and step, kPackSteps steps per tile; the reduction runs kReduceBlock
+// threads that each own kReduceSteps groups of 8 outputs.  One tile per
+// workgroup (small tiles, many workgroups) measured fastest for these HBM
+// streams.
 #ifndef FSDP_COPY_BLOCK
 #define FSDP_COPY_BLOCK 128
 #endif
@@ -22,6 +24,9 @@ namespace fsdp {
 #endif
 #ifndef FSDP_PACK_STEPS
 #define FSDP_PACK_STEPS 1
+#endif
+#ifndef FSDP_PACK_BLOCK
+#define FSDP_PACK_BLOCK 128
 #endif
 #ifndef FSDP_REDUCE_BLOCK
 #define FSDP_REDUCE_BLOCK 256
@@ -36,8 +41,9 @@ constexpr int64_t kCopyTile = int64_t(kCopyBlock) * kVec * kCopySteps;
 // The widening pack (bf16 in, fp32 out) moves 4 elements per thread and step,
 // so its tiles read half and write the same bytes as a copy tile.
 constexpr int64_t kWidenTile = int64_t(kCopyBlock) * 4 * kCopySteps;
+constexpr int kPackBlock = FSDP_PACK_BLOCK;
 constexpr int kPackSteps = FSDP_PACK_STEPS;
-constexpr int64_t kPackTile = int64_t(kCopyBlock) * kVec * kPackSteps;
+constexpr int64_t kPackTile = int64_t(kPackBlock) * kVec * kPackSteps;
 constexpr int kReduceBlock = FSDP_REDUCE_BLOCK;
 constexpr int kReduceSteps = FSDP_REDUCE_STEPS;
 constexpr int64_t kReduceTile = int64_t(kReduceBlock) * kVec * kReduceSteps;
@@ -53,6 +59,10 @@ struct Plan {
     std::vector<int64_t> seg;      // L_p
     std::vector<int64_t> off;      // off_p, with off[P] = S
     std::vector<int64_t> elems;    // N_p * inner_p
+    // Launch options fixed at planning (fsdp_plan_options); results never
+    // depend on them.
+    int64_t max_workgroups = 0;    // > 0: cap on every launch's grid
+    int32_t reduce_tiles = FSDP_REDUCE_TILES_AUTO;
 
     int64_t local_rows(int p, int r) const {
         int64_t c = cpr[p];

@@ -133,6 +133,45 @@ def test_planner_rejects(w, dims, align, code):
     assert LIB.fsdp_last_error()
 
 
+def raw_plan_ex(w, dims, options, align=8):
+    n = len(dims)
+    rows = (ctypes.c_int64 * n)(*[d[0] for d in dims])
+    inner = (ctypes.c_int64 * n)(*[d[1] for d in dims])
+    h = ctypes.c_void_p()
+    opts = None if options is None else ctypes.byref(native.PlanOptions(*options))
+    return LIB.fsdp_bucket_plan_ex(w, n, rows, inner, align, opts, ctypes.byref(h)), h
+
+
+@pytest.mark.parametrize("options,code", [
+    (None, OK),
+    ((0, 0, 0), OK),
+    ((7, 1, 0), OK),
+    ((1, 2, 0), OK),
+    ((-1, 0, 0), INVALID),
+    ((0, 3, 0), INVALID),
+    ((0, -1, 0), INVALID),
+    ((0, 0, 1), INVALID),
+])
+def test_plan_options(options, code):
+    """Launch options are checked at planning; a valid set gives the same plan."""
+    st_, h = raw_plan_ex(4, [(5, 3), (8, 2)], options)
+    assert st_ == code
+    if code == OK:
+        assert LIB.fsdp_plan_chunk_elems(h) == O.make_plan(4, [(5, 3), (8, 2)]).chunk
+        LIB.fsdp_plan_free(h)
+    else:
+        assert not h.value
+        assert LIB.fsdp_last_error()
+
+
+def test_plan_options_in_the_binding():
+    with pytest.raises(ValueError):
+        BucketPlan(4, [(5, 3)], reduce_tiles="quarter")
+    with pytest.raises(RuntimeError):
+        BucketPlan(4, [(5, 3)], max_workgroups=-2)
+    BucketPlan(4, [(5, 3)], max_workgroups=3, reduce_tiles="half").close()
+
+
 def test_plan_queries_on_bad_input():
     st_, h = raw_plan(4, [(5, 3)])
     assert st_ == OK
