@@ -6,7 +6,9 @@ nothing is written out of bounds).  Small buckets cover the edge cases (empty
 parameters, ranks holding no rows, W = 1, dim 0 smaller than W, 1-wide
 parameters, the dense align = 1 layout, element-aligned parameter pointers,
 the parameter limit, several tiles with ragged tails); the Llama-shaped
-workloads run at full size in the launch configuration the benchmark times.
+workloads, the 405B block included, run at full size in the launch
+configuration the benchmark times, with every output element compared, at
+ranks 0, W/2 and W-1 for the per-rank kernels.
 """
 
 from __future__ import annotations
@@ -123,15 +125,14 @@ def wide_bf16_host(words, n):
 
 # ----------------------------------------------------------------- small buckets
 
-@pytest.mark.parametrize("half", ["0", "1"])
-def test_reduce_tile_sizes(half, monkeypatch):
+@pytest.mark.parametrize("tiles", ["full", "half"])
+def test_reduce_tile_sizes(tiles):
     """The reduction with its tile size forced each way (full-size tiles of 256
     threads, half-size tiles of 128) on the small buckets, which otherwise
     take the half-size tiles: every output bit for bit."""
-    monkeypatch.setenv("FSDP_REDUCE_HALF_TILES", half)
     for case in range(len(SMALL)):
         w, dims = SMALL[case]
-        plan = BucketPlan(w, dims)
+        plan = BucketPlan(w, dims, reduce_tiles=tiles)
         oplan = O.make_plan(w, dims)
         recv = wide_bf16_host([case, 77], w * oplan.chunk)
         for r in _ranks(w):
@@ -141,13 +142,12 @@ def test_reduce_tile_sizes(half, monkeypatch):
 
 @pytest.mark.parametrize("cap", [1, 3, 50])
 @pytest.mark.parametrize("case", [3, 8, 10, 11])
-def test_grid_stride(case, cap, monkeypatch):
+def test_grid_stride(case, cap):
     """With the workgroup cap lowered, every workgroup loops over many tiles
     (of several parameters, and through the reduce's LDS staging more than
     once); the results stay bit-exact."""
-    monkeypatch.setenv("FSDP_MAX_WORKGROUPS", str(cap))
     w, dims = SMALL[case]
-    plan = BucketPlan(w, dims, 8)
+    plan = BucketPlan(w, dims, 8, max_workgroups=cap)
     oplan = O.make_plan(w, dims, 8)
     for r in _ranks(w):
         run_ag_pack(plan, oplan, r, seed=case)
@@ -331,90 +331,56 @@ def test_workload_full(key, kernel):
     elif kernel == "rs_pack":
         _full_rs_pack(plan, oplan, seed=key)
     else:
-        for r in sorted({0, W - 1}):
+        for r in _ranks(W):
             _full_rs_reduce(plan, oplan, r, seed=key * 10 + r)
     plan.close()
     torch.cuda.empty_cache()
 
 
-# ----------------------------------------------------------------- the 405B block, sampled
+# ----------------------------------------------------------------- the 405B block, in full
+#
+# W = 128, W*S = 3.19e9 elements (64-bit indexing; 6.4 GB per bucket buffer).
+# Every output element of every kernel is compared with the oracle; each
+# kernel is a test of its own so that one test's host copies are freed before
+# the next starts (about 20 GB of host memory at most).
 
-def _reader(t):
-    return lambda start, count: host_u16(t[start:start + count])
+W405 = WORKLOADS[4].world_size
 
 
-def test_workload_405b_sampled():
-    """405B block, W = 128 (W*S = 3.19e9 elements: 64-bit indexing).  ag_pack and
-    rs_reduce outputs are compared in full; ag_unpack and rs_pack outputs (6.4 GB
-    each) on sampled rows and ranges that include every rank-segment and
-    parameter boundary of the sampled ranks."""
+def _plans_405b():
     wl = WORKLOADS[4]
-    W = wl.world_size
-    plan = BucketPlan(W, wl.dims)
-    oplan = O.make_plan(W, wl.dims)
-    S = oplan.chunk
-    assert W * S > 2 ** 31
-    _full_ag_pack(plan, oplan, W - 1, seed=4)
+    plan = BucketPlan(wl.world_size, wl.dims)
+    oplan = O.make_plan(wl.world_size, wl.dims)
+    assert plan.chunk_elems == oplan.chunk
+    assert wl.world_size * oplan.chunk > 2 ** 31
+    return plan, oplan
 
-    rng = np.random.default_rng(405)
-    gathered = dev_random_bits16(W * S, 41)
-    outs = [torch.empty(n * k, dtype=torch.bfloat16, device=DEV) for n, k in wl.dims]
-    step("ag_unpack 405B")
-    plan.ag_unpack(gathered, outs)
-    torch.cuda.synchronize()
-    read = _reader(gathered)
-    for p, (n, k) in enumerate(wl.dims):
-        c = oplan.rows_per_rank[p]
-        rows = {0, n - 1}
-        for i in (0, 1, W // 2, W - 2, W - 1):
-            rows |= {min(n - 1, i * c), min(n - 1, i * c + c - 1)}
-        rows |= set(int(x) for x in rng.integers(0, n, 16))
-        rows = sorted(rows)
-        want = O.ag_unpack_rows(oplan, read, p, rows)
-        got = outs[p].view(n, k)[torch.tensor(rows, device=DEV)]
-        assert np.array_equal(host_u16(got).reshape(len(rows), k), want), p
-    del gathered, outs
-    torch.cuda.empty_cache()
 
-    grads = [dev_random_bits16(n * k, 4100 + p) for p, (n, k) in enumerate(wl.dims)]
-    send = Guarded(W * S, torch.bfloat16)
-    step("rs_pack 405B")
-    plan.rs_pack(grads, send.view)
-    torch.cuda.synchronize()
-    assert send.guards_intact()
-
-    def read_grad(p, lo, hi):
-        return host_u16(grads[p][lo:hi])
-
-    for j in (0, 1, W // 2, W - 1):
-        bounds = [0, S]
-        for p in range(oplan.num_params):
-            bounds += [oplan.offset[p], oplan.offset[p] + oplan.seg[p]]
-        for b in sorted(set(bounds)):
-            k0, k1 = max(0, b - 2048), min(S, b + 2048)
-            got = host_u16(send.view[j * S + k0:j * S + k1])
-            assert np.array_equal(got, O.rs_pack_range(oplan, read_grad, j, k0, k1)), (j, b)
-        for k0 in rng.integers(0, S - 65536, 4):
-            k0 = int(k0)
-            got = host_u16(send.view[j * S + k0:j * S + k0 + 65536])
-            assert np.array_equal(got, O.rs_pack_range(oplan, read_grad, j, k0, k0 + 65536)), (j, k0)
-    del grads, send
-    torch.cuda.empty_cache()
-
-    for r in (0, W - 1):
-        recv = dev_wide_bf16(W * S, 4200 + r)
-        outs = [torch.empty(O.local_elems(oplan, p, r), dtype=torch.float32, device=DEV)
-                for p in range(oplan.num_params)]
-        step(f"rs_reduce 405B rank={r}")
-        plan.rs_reduce(r, recv, outs)
-        torch.cuda.synchronize()
-        rd = _reader(recv)
-        for p in range(oplan.num_params):
-            v = O.local_elems(oplan, p, r)
-            for e0 in sorted({0, max(0, v - 4096)} | set(int(x) for x in rng.integers(0, max(1, v - 4096), 3))):
-                e1 = min(v, e0 + 4096)
-                want = O.rs_reduce_range(oplan, r, rd, p, e0, e1)
-                assert np.array_equal(host_u32(outs[p][e0:e1]), want.view(np.uint32)), (r, p, e0)
-        del recv, outs
-        torch.cuda.empty_cache()
+@pytest.mark.parametrize("rank", _ranks(W405))
+def test_workload_405b_ag_pack(rank):
+    plan, oplan = _plans_405b()
+    _full_ag_pack(plan, oplan, rank, seed=4)
     plan.close()
+    torch.cuda.empty_cache()
+
+
+def test_workload_405b_ag_unpack():
+    plan, oplan = _plans_405b()
+    _full_ag_unpack(plan, oplan, seed=41)
+    plan.close()
+    torch.cuda.empty_cache()
+
+
+def test_workload_405b_rs_pack():
+    plan, oplan = _plans_405b()
+    _full_rs_pack(plan, oplan, seed=42)
+    plan.close()
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("rank", _ranks(W405))
+def test_workload_405b_rs_reduce(rank):
+    plan, oplan = _plans_405b()
+    _full_rs_reduce(plan, oplan, rank, seed=4200 + rank)
+    plan.close()
+    torch.cuda.empty_cache()

@@ -91,9 +91,9 @@ def _wide_f32(words, n):
 
 @pytest.mark.parametrize("case", range(len(CASES)))
 @pytest.mark.parametrize("align", [8, 1])
-def test_ex_small(case, align):
+def test_ex_small(case, align, max_workgroups=0):
     W, dims = CASES[case]
-    plan = BucketPlan(W, dims, align)
+    plan = BucketPlan(W, dims, align, max_workgroups=max_workgroups)
     oplan = O.make_plan(W, dims, align)
     S = oplan.chunk
     P = len(dims)
@@ -177,12 +177,12 @@ def test_ex_small(case, align):
 
 
 @pytest.mark.parametrize("case", range(len(CASES)))
-def test_ag_pack_push(case):
+def test_ag_pack_push(case, max_workgroups=0):
     """The packed chunk of one rank written to W separate destinations, bf16
     and fp32: every destination equals the oracle's pack."""
     W, dims = CASES[case]
     for align in (8, 1):
-        plan = BucketPlan(W, dims, align)
+        plan = BucketPlan(W, dims, align, max_workgroups=max_workgroups)
         oplan = O.make_plan(W, dims, align)
         S = oplan.chunk
         P = len(dims)
@@ -231,20 +231,18 @@ def test_push_destination_rows(W):
 
 
 @pytest.mark.parametrize("cap", [1, 7])
-def test_ex_grid_stride(cap, monkeypatch):
+def test_ex_grid_stride(cap):
     """The element-type and chunk-table forms with every workgroup looping over
     many tiles."""
-    monkeypatch.setenv("FSDP_MAX_WORKGROUPS", str(cap))
-    test_ex_small(5, 8)
+    test_ex_small(5, 8, max_workgroups=cap)
 
 
 @pytest.mark.parametrize("cap", [1, 7, 50])
-def test_push_grid_stride(cap, monkeypatch):
+def test_push_grid_stride(cap):
     """The push at W = 48 (a pack and a copy) with every workgroup looping over
     many work items, including caps that are not a multiple of the XCD count."""
-    monkeypatch.setenv("FSDP_MAX_WORKGROUPS", str(cap))
     assert CASES[4][0] == 48
-    test_ag_pack_push(4)
+    test_ag_pack_push(4, max_workgroups=cap)
 
 
 def test_ex_chunks_alias_one_buffer():
