@@ -13,11 +13,16 @@ distributions (params N(0, 0.02) with RMSNorm weights 1.0, grads N(0, 1e-3)
 in bf16), generated on the device before timing and resident in HBM.  The
 metric is effective HBM bandwidth: the algorithmic bytes of the step (what
 the method must read and write, padding writes included) divided by the
-step time.  Per-kernel launch durations come from HIP events recorded on the
-stream the kernels run on; the dominant kernel's figure is the roofline
-entry.  A plain device-to-device copy of the unpack's bytes is timed beside
-them as the achievable reference.  The CPU oracle is timed on a bounded
-sample of the same workload.
+step time.  HIP events recorded on the stream the kernels run on time every
+kernel inside the steps; the kernel with the longest launches gives the
+roofline entry.  A per-kernel leg then launches each call 30 times over
+rotating input/output sets of more than 1.5 GiB (so no launch finds its data
+in the caches), with the device kept busy while the host enqueues them, and
+reports the median and minimum by HIP events and, from a child run of the same
+leg under a rocprofv3 kernel trace, by the kernels' own start and end
+timestamps.  A plain device-to-device copy of the unpack's bytes is timed
+beside them as the achievable reference.  The CPU oracle is timed on a
+bounded sample of the same workload.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 3] [--rank 0]
 """
@@ -39,17 +44,30 @@ if ROOT not in sys.path:
 METRIC = "effective HBM GB/s (and % of peak) for bucket pack/unpack/reduce"
 PEAK_GBPS = 8000.0                       # MI355X HBM3E
 KERNELS = ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")
-# device symbols of the kernels each call launches (bf16 wire, one contiguous
-# buffer); rocprofv3 reports them by these names.  A small rank shard (fewer
-# than 4 full-size tiles per CU) reduces with 128-thread workgroups instead.
+# Device symbols of the kernels each call launches (bf16 wire, one contiguous
+# buffer), as rocprofv3 prints them; a kernel trace taken during the run
+# replaces these with the names it saw.  A rank shard of fewer than 4
+# full-size reduce tiles per CU is reduced with 128-thread workgroups.
 KERNEL_SYMBOLS = {
     "ag_pack": "ag_pack_kernel<1, OneChunk>",
     "ag_unpack": "ag_unpack_kernel<ContigChunks>",
     "rs_pack": "rs_pack_kernel<ContigChunks, 0>",
     "rs_reduce": "rs_reduce_kernel<ContigChunks, unsigned short, 256>",
 }
+REDUCE_SMALL_SYMBOL = "rs_reduce_kernel<ContigChunks, unsigned short, 128>"
+KERNEL_BASENAMES = ("ag_pack_kernel", "ag_unpack_kernel", "rs_pack_kernel", "rs_reduce_kernel", "probe_read_kernel",
+                    "probe_fill_kernel", "probe_copy_kernel", "probe_cast_kernel", "probe_reduce_kernel")
+PROBES_LIB = os.path.join(ROOT, "paper_2411_00284_amd", "libfsdp_probes.so")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_00284_amd", "csrc", "bucket_kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
+# The per-kernel leg cycles through input/output sets that together hold more
+# than this many bytes, so that no launch finds its data in the L2 caches or
+# the 256 MB Infinity Cache.
+ROTATE_BYTES = 3 << 29
+SLEEP_CYCLES = 50_000_000                # a device-side wait that lets the host enqueue a whole leg
+# The full-size reduce tile and the small-shard threshold of the library.
+REDUCE_TILE = 256 * 8 * 2
+SMALL_SHARD_TILES_PER_CU = 4
 
 
 def algorithmic_bytes(W, S, E, V0):
@@ -62,6 +80,15 @@ def algorithmic_bytes(W, S, E, V0):
     }
 
 
+def kernel_symbol(name, plan, rank, cus):
+    """The symbol the call launches for this plan and rank."""
+    if name == "rs_reduce":
+        full_tiles = sum(-(-plan.local_elems(p, rank) // REDUCE_TILE) for p in range(plan.num_params))
+        if full_tiles < SMALL_SHARD_TILES_PER_CU * cus:
+            return REDUCE_SMALL_SYMBOL
+    return KERNEL_SYMBOLS[name]
+
+
 def kernel_source_sha():
     with open(KERNEL_SOURCE, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
@@ -70,8 +97,7 @@ def kernel_source_sha():
 def read_profile_avg_us(kernel: str, workload: str):
     """The kernel's average duration in the committed rocprofv3 summary of the
     same workload, or None when there is none or the kernel source changed
-    since it was taken (event timing reads short kernels long; this is the
-    kernel's own duration)."""
+    since it was taken."""
     path = os.path.join(PROFILES, f"kernels_{workload}_stats.md")
     if not os.path.exists(path):
         return None
@@ -97,6 +123,371 @@ def read_traffic(kernel: str, workload: str):
     return float(m.group(1)) if m else None
 
 
+def stats_us(ms_list):
+    """Median, minimum and mean of launch times given in ms, in us."""
+    import numpy as np
+    a = np.asarray(ms_list, dtype=np.float64) * 1e3
+    return {"median_us": round(float(np.median(a)), 3), "min_us": round(float(a.min()), 3),
+            "mean_us": round(float(a.mean()), 3)}
+
+
+# ----------------------------------------------------------------- per-kernel leg
+
+def kernel_set(name, plan, wl, rank, dev, gen):
+    """One input/output set of a kernel's call at ``rank``: returns the call
+    (taking a stream) and the tensors it keeps alive.  Values follow the
+    workload recipe (params N(0, 0.02), norms 1.0, bf16 N(0, 1e-3) grads)."""
+    import torch
+
+    S, W, P = plan.chunk_elems, plan.world_size, plan.num_params
+
+    def normal(n, scale, dtype):
+        out = torch.empty(n, dtype=dtype, device=dev)
+        step_n = 1 << 27
+        for s in range(0, n, step_n):
+            e = min(n, s + step_n)
+            out[s:e] = (torch.randn(e - s, generator=gen, device=dev) * scale).to(dtype)
+        return out
+
+    if name == "ag_pack":
+        shards = [torch.ones(plan.local_elems(p, rank), device=dev) if wl.is_norm[p]
+                  else normal(plan.local_elems(p, rank), 0.02, torch.float32) for p in range(P)]
+        out = torch.empty(S, dtype=torch.bfloat16, device=dev)
+        return (lambda st: plan.ag_pack(rank, shards, out, st)), (shards, out)
+    if name == "ag_unpack":
+        gathered = normal(W * S, 0.02, torch.bfloat16)
+        params = [torch.empty(n * k, dtype=torch.bfloat16, device=dev) for n, k in wl.dims]
+        return (lambda st: plan.ag_unpack(gathered, params, st)), (gathered, params)
+    if name == "rs_pack":
+        grads = [normal(n * k, 1e-3, torch.bfloat16) for n, k in wl.dims]
+        send = torch.empty(W * S, dtype=torch.bfloat16, device=dev)
+        return (lambda st: plan.rs_pack(grads, send, st)), (grads, send)
+    recv = normal(W * S, 1e-3, torch.bfloat16)
+    outs = [torch.empty(plan.local_elems(p, rank), dtype=torch.float32, device=dev) for p in range(P)]
+    return (lambda st: plan.rs_reduce(rank, recv, outs, st)), (recv, outs)
+
+
+def time_launches(calls, reps, stream, labels=None, label=None, warm=3):
+    """``reps`` launches cycling through ``calls`` (one per input/output set),
+    after ``warm`` untimed ones, with the device kept busy by a wait kernel
+    while the host enqueues them all: the HIP events then see device time
+    only.  Returns the per-launch times (event pairs between consecutive
+    launches, ms) and the average over all of them back to back (one pair)."""
+    import torch
+
+    n = len(calls)
+    for k in range(max(warm, 1)):
+        calls[k % n](stream)
+        if labels is not None:
+            labels.append(label)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    with torch.cuda.stream(stream):
+        torch.cuda._sleep(SLEEP_CYCLES)
+    ev[0].record(stream)
+    for k in range(reps):
+        calls[k % n](stream)
+        ev[k + 1].record(stream)
+        if labels is not None:
+            labels.append(label)
+    torch.cuda.synchronize()
+    per = [ev[k].elapsed_time(ev[k + 1]) for k in range(reps)]
+    return per, ev[0].elapsed_time(ev[reps]) / reps
+
+
+def kernel_leg(plan, wl, rank, reps, dev, stream, labels=None):
+    """Each of the four calls ``reps`` times over rotating input/output sets
+    of more than ROTATE_BYTES in total; per kernel: event statistics."""
+    import torch
+
+    W, S, E = plan.world_size, plan.chunk_elems, wl.total_elems
+    V0 = sum(plan.local_elems(p, rank) for p in range(plan.num_params))
+    abytes = algorithmic_bytes(W, S, E, V0)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2000 + wl.key)
+    res = {}
+    for name in KERNELS:
+        nsets = min(64, max(2, -(-ROTATE_BYTES // abytes[name])))
+        sets = [kernel_set(name, plan, wl, rank, dev, gen) for _ in range(nsets)]
+        torch.cuda.synchronize()
+        per, b2b = time_launches([c for c, _ in sets], reps, stream, labels, name, warm=min(nsets, 8))
+        res[name] = {"reps": reps, "sets": nsets, "set_bytes": abytes[name], **{
+            "event_" + k: v for k, v in stats_us(per).items()}, "b2b_avg_us": round(b2b * 1e3, 3)}
+        del sets
+        torch.cuda.empty_cache()
+    return res
+
+
+# ----------------------------------------------------------------- ceilings: reference streams
+
+CEILINGS = ("probe_read", "probe_fill", "probe_copy", "probe_cast", "probe_reduce_store", "probe_reduce_nostore")
+
+
+def load_probes():
+    """The reference-stream library (built beside the bucket library)."""
+    import ctypes
+
+    import torch  # noqa: F401  (the probes bind to torch's HIP runtime)
+
+    if not os.path.exists(PROBES_LIB):
+        raise ImportError(f"{PROBES_LIB} is not built: run `python -m paper_2411_00284_amd.build`")
+    lib = ctypes.CDLL(PROBES_LIB)
+    i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+    sigs = {"probe_read": [vp, i64, vp, vp], "probe_fill": [vp, i64, vp], "probe_copy": [vp, vp, i64, vp],
+            "probe_cast": [vp, vp, i64, vp], "probe_strided_reduce": [vp, i64, i32, vp, i64, i32, vp, vp]}
+    for name, args in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    return lib
+
+
+def ceiling_bytes(plan, rank):
+    """Bytes each reference stream moves at the bucket's shapes: the W*S
+    buffer read, filled and copied; the rank's fp32 shard elements cast; the
+    rank's outputs (whole 4096-element tiles) reduced over W strided sources,
+    with and without storing them."""
+    W, S = plan.world_size, plan.chunk_elems
+    V0 = sum(plan.local_elems(p, rank) for p in range(plan.num_params))
+    n4 = V0 // 4
+    nr = V0 // 4096 * 4096
+    return {"probe_read": 2 * W * S, "probe_fill": 2 * W * S, "probe_copy": 4 * W * S, "probe_cast": 24 * n4,
+            "probe_reduce_store": 2 * W * nr + 4 * nr, "probe_reduce_nostore": 2 * W * nr}
+
+
+def ceiling_set(name, plan, rank, dev, gen, lib, sink):
+    """One input/output set of a reference stream; returns its call and tensors."""
+    import torch
+
+    W, S = plan.world_size, plan.chunk_elems
+    V0 = sum(plan.local_elems(p, rank) for p in range(plan.num_params))
+
+    def check(rc):
+        if rc != 0:
+            raise RuntimeError(f"{name}: HIP error {rc}")
+
+    if name in ("probe_read", "probe_fill", "probe_copy"):
+        src = torch.randn(W * S, generator=gen, device=dev).to(torch.bfloat16)
+        n16 = W * S * 2 // 16
+        if name == "probe_read":
+            return (lambda st: check(lib.probe_read(src.data_ptr(), n16, sink.data_ptr(), st.cuda_stream))), (src,)
+        if name == "probe_fill":
+            return (lambda st: check(lib.probe_fill(src.data_ptr(), n16, st.cuda_stream))), (src,)
+        dst = torch.empty_like(src)
+        return (lambda st: check(lib.probe_copy(src.data_ptr(), dst.data_ptr(), n16, st.cuda_stream))), (src, dst)
+    if name == "probe_cast":
+        n4 = V0 // 4
+        src = torch.randn(4 * n4, generator=gen, device=dev) * 0.02
+        dst = torch.empty(4 * n4, dtype=torch.bfloat16, device=dev)
+        return (lambda st: check(lib.probe_cast(src.data_ptr(), dst.data_ptr(), n4, st.cuda_stream))), (src, dst)
+    nr = V0 // 4096 * 4096
+    store = 1 if name == "probe_reduce_store" else 0
+    src = (torch.randn(W * S, generator=gen, device=dev) * 1e-3).to(torch.bfloat16)
+    dst = torch.empty(max(nr, 4), dtype=torch.float32, device=dev)
+    return (lambda st: check(lib.probe_strided_reduce(src.data_ptr(), S, W, dst.data_ptr(), nr, store,
+                                                       sink.data_ptr(), st.cuda_stream))), (src, dst)
+
+
+def ceiling_leg(plan, rank, reps, dev, stream, labels=None):
+    """Each reference stream ``reps`` times over rotating sets, as the
+    per-kernel leg times the library's calls."""
+    import torch
+
+    lib = load_probes()
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(4000)
+    nbytes = ceiling_bytes(plan, rank)
+    res = {}
+    for name in CEILINGS:
+        if nbytes[name] == 0:
+            continue
+        nsets = min(64, max(2, -(-ROTATE_BYTES // nbytes[name])))
+        sets = [ceiling_set(name, plan, rank, dev, gen, lib, sink) for _ in range(nsets)]
+        torch.cuda.synchronize()
+        per, b2b = time_launches([c for c, _ in sets], reps, stream, labels, name, warm=min(nsets, 8))
+        res[name] = {"bytes": nbytes[name], "sets": nsets, **{"event_" + k: v for k, v in stats_us(per).items()},
+                     "b2b_avg_us": round(b2b * 1e3, 3)}
+        del sets
+        torch.cuda.empty_cache()
+    return res
+
+
+# ----------------------------------------------------------------- kernel trace of a child run
+
+def short_symbol(name):
+    """A trace's kernel name without return type, namespaces or parameter list."""
+    name = name.replace("(anonymous namespace)::", "").replace("fsdp::", "")
+    if name.startswith("void "):
+        name = name[5:]
+    depth = 0
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return name[:i].strip()
+    return name.strip()
+
+
+def rocprof_path():
+    import shutil
+    return shutil.which("rocprofv3") or ("/opt/rocm/bin/rocprofv3" if os.path.exists("/opt/rocm/bin/rocprofv3")
+                                         else None)
+
+
+def traced_child(spec, timeout=600):
+    """Run ``bench.py --child`` with ``spec`` as a child process under
+    ``rocprofv3 --kernel-trace`` and return (child result, per-launch kernel
+    durations in ms grouped by the child's labels, kernel names per label), or
+    (None, None, reason).  The child labels every library launch it makes, in
+    order; the trace's dispatches of the library kernels are matched to them
+    one to one."""
+    import csv
+    import glob
+    import shutil
+    import subprocess
+    import tempfile
+
+    prof = rocprof_path()
+    if prof is None:
+        return None, None, "rocprofv3 not found"
+    tmp = tempfile.mkdtemp(prefix="bench_trace_")
+    try:
+        spec_path = os.path.join(tmp, "spec.json")
+        out_path = os.path.join(tmp, "child.json")
+        with open(spec_path, "w") as f:
+            json.dump(spec, f)
+        cmd = [prof, "--kernel-trace", "-f", "csv", "-d", os.path.join(tmp, "trace"), "-o", "trace", "--",
+               sys.executable, os.path.abspath(__file__), "--child", spec_path, out_path]
+        env = dict(os.environ, TMPDIR=tmp)
+        try:
+            res = subprocess.run(cmd, cwd=tmp, env=env, capture_output=True, text=True, timeout=timeout)
+        except subprocess.TimeoutExpired:
+            return None, None, "traced child run timed out"
+        csvs = glob.glob(os.path.join(tmp, "trace", "**", "*kernel_trace.csv"), recursive=True)
+        if not os.path.exists(out_path) or not csvs:
+            return None, None, f"traced child run failed (rc {res.returncode}): {res.stderr[-400:]}"
+        child = json.load(open(out_path))
+        rows = []
+        with open(csvs[0]) as f:
+            for r in csv.DictReader(f):
+                name = r["Kernel_Name"]
+                if any(b in name for b in KERNEL_BASENAMES):
+                    key = int(r.get("Dispatch_Id") or 0), int(r["Start_Timestamp"])
+                    rows.append((key, (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-6, name))
+        rows.sort()
+        labels = child["labels"]
+        if len(rows) != len(labels):
+            return None, None, f"{len(rows)} library dispatches traced for {len(labels)} launches"
+        per, names = {}, {}
+        for (_, ms, name), lab in zip(rows, labels):
+            per.setdefault(lab, []).append(ms)
+            names.setdefault(lab, short_symbol(name))
+        return child, per, names
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+
+
+def child_main(spec_path, out_path):
+    """The traced child: runs the leg the spec names and writes its labels."""
+    import torch
+
+    from paper_2411_00284_amd import BucketPlan
+    from synth import workload
+
+    spec = json.load(open(spec_path))
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    labels = []
+    out = {"spec": spec}
+    if spec["mode"] == "kernels":
+        wl = workload(spec["workload"])
+        plan = BucketPlan(wl.world_size, wl.dims)
+        out["events"] = kernel_leg(plan, wl, spec["rank"], spec["reps"], dev, stream, labels)
+        if spec.get("ceilings"):
+            out["ceilings"] = ceiling_leg(plan, spec["rank"], spec["reps"], dev, stream, labels)
+        plan.close()
+    elif spec["mode"] == "pack_sweep":
+        out["cases"] = pack_sweep_leg(spec["reps"], dev, stream, labels)
+    out["labels"] = labels
+    with open(out_path, "w") as f:
+        json.dump(out, f)
+    return 0
+
+
+# ----------------------------------------------------------------- ag_pack over bucket sizes
+
+def pack_sweep_cases():
+    """Buckets for the pack's size sweep: one Llama-3 block (8B, 70B, 405B
+    shapes) at several world sizes, so one rank's chunk spans 10 to 320 MB of
+    algorithmic bytes, plus one-parameter buckets of 1, 64 and 512 tiles for
+    the fixed cost of a launch."""
+    from synth.workloads import KV_ROWS, Workload, _block
+
+    blocks = {"8b": (4096, 14336), "70b": (8192, 28672), "405b": (16384, 53248)}
+    cases = [Workload(0, f"one-param-{t}-tiles", 1, ("x",), ((t * 1024, 1),), (False,)) for t in (1, 64, 512)]
+    for blk, w in (("8b", 128), ("8b", 64), ("70b", 128), ("8b", 32), ("70b", 64), ("8b", 16), ("405b", 128),
+                   ("70b", 32), ("8b", 8), ("405b", 64), ("70b", 16)):
+        d, f = blocks[blk]
+        cases.append(_block(0, f"llama3-{blk}-block-w{w}", w, d, f, KV_ROWS))
+    return cases
+
+
+def pack_sweep_leg(reps, dev, stream, labels):
+    import torch
+
+    from paper_2411_00284_amd import BucketPlan
+
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(3000)
+    res = []
+    for wl in pack_sweep_cases():
+        plan = BucketPlan(wl.world_size, wl.dims)
+        S = plan.chunk_elems
+        V0 = sum(plan.local_elems(p, 0) for p in range(wl.num_params))
+        nbytes = 4 * V0 + 2 * S
+        nsets = min(200, max(2, -(-ROTATE_BYTES // nbytes)))
+        sets = [kernel_set("ag_pack", plan, wl, 0, dev, gen) for _ in range(nsets)]
+        torch.cuda.synchronize()
+        per, b2b = time_launches([c for c, _ in sets], reps, stream, labels, wl.name, warm=min(nsets, 8))
+        res.append({"name": wl.name, "world_size": wl.world_size, "bytes": nbytes, "sets": nsets,
+                    **{"event_" + k: v for k, v in stats_us(per).items()}, "b2b_avg_us": round(b2b * 1e3, 3)})
+        del sets
+        plan.close()
+        torch.cuda.empty_cache()
+    return res
+
+
+def pack_sweep(reps):
+    """The pack over pack_sweep_cases(), timed by a live kernel trace; fits
+    T = t0 + bytes / BW to the trace medians of the block buckets and reports
+    the one-parameter buckets' median as the launch floor."""
+    import numpy as np
+
+    child, per, names = traced_child({"mode": "pack_sweep", "reps": reps})
+    if child is None:
+        return {"error": names}
+    rows = []
+    for c in child["cases"]:
+        d = per[c["name"]][-reps:]
+        st = stats_us(d)
+        rows.append({**c, **{"rocprof_" + k: v for k, v in st.items()},
+                     "GBps_rocprof_median": round(c["bytes"] / (st["median_us"] * 1e-6) / 1e9, 1)})
+    blocks = [r for r in rows if r["name"].startswith("llama3")]
+    x = np.array([r["bytes"] for r in blocks], dtype=np.float64)
+    y = np.array([r["rocprof_median_us"] for r in blocks], dtype=np.float64)
+    beta, t0 = np.polyfit(x, y, 1)
+    r2 = 1.0 - float(np.sum((y - (t0 + beta * x)) ** 2) / np.sum((y - y.mean()) ** 2))
+    floor = float(np.median([r["rocprof_median_us"] for r in rows if r["name"].startswith("one-param")]))
+    return {"kernel": names.get(blocks[0]["name"]), "reps": reps, "cases": rows,
+            "fit": {"t0_us": round(float(t0), 3), "GBps": round(1e-3 / float(beta), 1), "r2": round(r2, 5),
+                    "points": len(blocks)},
+            "launch_floor_us": round(floor, 3)}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -110,6 +501,14 @@ def main(argv=None):
     ap.add_argument("--variant-reps", type=int, default=10)
     ap.add_argument("--event-every", type=int, default=5,
                     help="record the per-kernel HIP events on every N-th timed step (N=1: every step)")
+    ap.add_argument("--kernel-reps", type=int, default=30,
+                    help="launches per kernel in the per-kernel leg (rotating sets, device kept ahead)")
+    ap.add_argument("--no-trace", action="store_true",
+                    help="skip the per-kernel leg's rocprofv3 kernel trace (a child run)")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="also time reference streams (read, fill, copy, cast, strided reduce) at the bucket's shapes")
+    ap.add_argument("--pack-sweep", action="store_true",
+                    help="also time ag_pack over buckets of 10-320 MB by kernel trace and fit t0 + bytes/BW")
     ap.add_argument("--copy-cost", action="store_true",
                     help="also fit the alpha + beta*bytes copy cost over sub-buckets of the block "
                          "(launches the path kernels at other sizes, so it is off in profiled runs)")
@@ -117,8 +516,11 @@ def main(argv=None):
                     help="also time the step replayed from a HIP graph")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the steps, run a plain 1 GiB device copy (for counter scaling)")
+    ap.add_argument("--child", nargs=2, metavar=("SPEC", "OUT"), help=argparse.SUPPRESS)
     args = ap.parse_args(argv)
 
+    if args.child:
+        return child_main(*args.child)
     if args.gpus != 1:
         print(f"bench.py: one GPU only (asked for --gpus {args.gpus}); "
               "the path has no collective and runs per rank", file=sys.stderr)
@@ -135,13 +537,39 @@ def main(argv=None):
     if not 0 <= rank < W:
         print(f"bench.py: --rank {rank} is outside 0..{W - 1} for {wl.name}", file=sys.stderr)
         return 2
+
+    # The per-kernel leg under a kernel trace runs first, in a child process,
+    # before this process allocates its own buffers.
+    reps = max(1, args.kernel_reps)
+    trace = None
+    if not args.no_trace:
+        child, per, names = traced_child({"mode": "kernels", "workload": args.workload, "rank": rank, "reps": reps,
+                                          "ceilings": args.ceilings})
+        trace = {"error": names} if child is None else {
+            name: {"symbol": names[name], **{"rocprof_" + k: v for k, v in stats_us(per[name][-reps:]).items()}}
+            for name in per}
+
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
     plan = BucketPlan(W, wl.dims)
     S = plan.chunk_elems
     P = wl.num_params
     E = wl.total_elems
     V0 = sum(plan.local_elems(p, rank) for p in range(P))
+    stream = torch.cuda.current_stream()
+
+    # ---- the per-kernel leg: each call over rotating sets of > 1.5 GiB
+    leg = kernel_leg(plan, wl, rank, reps, dev, stream)
+    ceilings = None
+    if args.ceilings:
+        ceilings = ceiling_leg(plan, rank, reps, dev, stream)
+        for name, c in ceilings.items():
+            tr = trace.get(name) if trace and "error" not in trace else None
+            us = tr["rocprof_median_us"] if tr else c["event_median_us"]
+            c["trace"] = tr
+            c["GBps"] = round(c["bytes"] / (us * 1e-6) / 1e9, 1)
+            c["frac"] = round(c["bytes"] / (us * 1e-6) / 1e9 / PEAK_GBPS, 4)
 
     # ---- seeded synthetic inputs, resident in HBM before timing
     g = torch.Generator(device=dev)
@@ -167,8 +595,6 @@ def main(argv=None):
     recv = normal(W * S, 1e-3, torch.bfloat16)
     outs = [torch.empty(plan.local_elems(p, rank), dtype=torch.float32, device=dev) for p in range(P)]
     torch.cuda.synchronize()
-
-    stream = torch.cuda.current_stream()
 
     def run_step(ev=None, st=None):
         st = stream if st is None else st
@@ -214,12 +640,23 @@ def main(argv=None):
     kernels = {}
     for name in KERNELS:
         avg_ms = float(np.mean(per_kernel_ms[name]))
-        gbps = abytes[name] / (avg_ms * 1e-3) / 1e9
-        kernels[name] = {"avg_us": round(avg_ms * 1e3, 2),
-                         "median_us": round(float(np.median(per_kernel_ms[name])) * 1e3, 2),
-                         "min_us": round(float(np.min(per_kernel_ms[name])) * 1e3, 2),
-                         "bytes": abytes[name], "GBps": round(gbps, 1), "frac": round(gbps / PEAK_GBPS, 4),
-                         "rocprof_avg_us": read_profile_avg_us(name, wl.name)}
+        lg = leg[name]
+        tr = trace.get(name) if trace and "error" not in trace else None
+        kernel_us = tr["rocprof_median_us"] if tr else lg["event_median_us"]
+        gbps = abytes[name] / (kernel_us * 1e-6) / 1e9
+        kernels[name] = {
+            "symbol": tr["symbol"] if tr else kernel_symbol(name, plan, rank, cus),
+            "bytes": abytes[name],
+            "GBps": round(gbps, 1), "frac": round(gbps / PEAK_GBPS, 4),
+            "timing": "rocprofv3 kernel trace median (live)" if tr else "HIP event median",
+            "leg": lg,
+            "leg_frac_event_median": round(abytes[name] / (lg["event_median_us"] * 1e-6) / 1e9 / PEAK_GBPS, 4),
+            "trace": tr,
+            "step_event_avg_us": round(avg_ms * 1e3, 2),
+            "step_event_median_us": round(float(np.median(per_kernel_ms[name])) * 1e3, 2),
+            "step_event_samples": len(per_kernel_ms[name]),
+            "committed_rocprof_avg_us": read_profile_avg_us(name, wl.name),
+        }
 
     copy_ref = None if args.no_variants else time_d2d_copy(gathered, send_buf, stream, args.variant_reps)
 
@@ -236,15 +673,18 @@ def main(argv=None):
         torch.cuda.synchronize()
         del a, b
 
-    dominant = max(KERNELS, key=lambda n: kernels[n]["avg_us"])
+    # The roofline entry: the kernel with the longest launches in the timed
+    # steps, at its HIP-event average over those steps.
+    dominant = max(KERNELS, key=lambda n: kernels[n]["step_event_avg_us"])
     dom = kernels[dominant]
+    dom_gbps = abytes[dominant] / (dom["step_event_avg_us"] * 1e-6) / 1e9
     roofline = {
         "bound": "hbm",
-        "kernel": KERNEL_SYMBOLS[dominant],
-        "achieved": dom["GBps"],
+        "kernel": dom["symbol"],
+        "achieved": round(dom_gbps, 1),
         "peak": PEAK_GBPS,
         "unit": "GB/s",
-        "frac": dom["frac"],
+        "frac": round(dom_gbps / PEAK_GBPS, 4),
         "traffic": read_traffic(dominant, wl.name),
     }
 
@@ -271,7 +711,8 @@ def main(argv=None):
                    "step": "ag_pack+ag_unpack+rs_pack+rs_reduce", "step_bytes": step_bytes},
         "frac_of_peak": round(step_bytes / (elapsed / args.steps) / 1e9 / PEAK_GBPS, 4),
         "kernels": kernels,
-        "kernel_event_steps": len(per_kernel_ms[KERNELS[0]]),
+        "kernel_trace": trace.get("error") if trace and "error" in trace else (
+            None if trace is None else "rocprofv3 --kernel-trace of the per-kernel leg in a child process"),
         "roofline": roofline,
         "d2d_copy": copy_ref,
         "cpu_baseline": cpu,
@@ -280,6 +721,8 @@ def main(argv=None):
         "copy_cost": fit_copy_cost(wl, stream) if args.copy_cost else None,
         "graph": None if not args.graph else time_graph_step(
             lambda: run_step(None, torch.cuda.current_stream()), args.steps),
+        "ceilings": ceilings,
+        "pack_sweep": pack_sweep(reps) if args.pack_sweep else None,
     }
     print(json.dumps(line), flush=True)
     plan.close()

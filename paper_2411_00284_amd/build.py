@@ -22,6 +22,9 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB_NAME = "libfsdp_bucket.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
+# Reference streams for the benchmark's ceiling leg: a library of their own,
+# not loaded by the package.
+PROBES_PATH = os.path.join(PKG, "libfsdp_probes.so")
 
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
@@ -60,6 +63,11 @@ def build(verbose: bool = False) -> str:
     tmp = LIB_PATH + f".tmp{os.getpid()}"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, kobj, *hobjs], verbose)
     os.replace(tmp, LIB_PATH)
+    pobj = os.path.join(BUILD, "ceiling_probes.o")
+    _run([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, "ceiling_probes.hip"), "-o", pobj], verbose)
+    tmp = PROBES_PATH + f".tmp{os.getpid()}"
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, pobj], verbose)
+    os.replace(tmp, PROBES_PATH)
     return LIB_PATH
 
 

@@ -21,7 +21,7 @@ def test_bench_line_on_the_toy_block():
     print("bench.py --workload 1 --steps 3 --warmup 1", flush=True)
     res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "1", "--steps", "3",
                           "--warmup", "1", "--variant-reps", "1", "--event-every", "1"],
-                         capture_output=True, text=True, timeout=110)
+                         capture_output=True, text=True, timeout=240)
     assert res.returncode == 0, res.stderr[-2000:]
     lines = [l for l in res.stdout.splitlines() if l.startswith("{")]
     assert len(lines) == 1
@@ -42,4 +42,16 @@ def test_bench_line_on_the_toy_block():
     # the library on the oracle's own inputs, compared bit for bit inside the bench
     assert cpu["parity"] == {"ag_pack": True, "ag_unpack": True, "rs_pack": True, "rs_reduce": True}
     assert set(d["kernels"]) == {"ag_pack", "ag_unpack", "rs_pack", "rs_reduce"}
+    # the per-kernel leg: >= 30 launches per kernel over rotating sets of more
+    # than 1.5 GiB (or the 64-set cap), timed by events and by a kernel trace
+    for name, k in d["kernels"].items():
+        leg = k["leg"]
+        assert leg["reps"] >= 30 and leg["sets"] >= 2
+        assert leg["sets"] * leg["set_bytes"] > 3 << 29 or leg["sets"] == 64
+        assert 0 < leg["event_min_us"] <= leg["event_median_us"]
+        assert k["symbol"].startswith(name + "_kernel<"), k["symbol"]
+        if k["trace"] is not None:
+            assert 0 < k["trace"]["rocprof_min_us"] <= k["trace"]["rocprof_median_us"]
+            assert k["timing"].startswith("rocprofv3")
+    assert d["kernel_trace"] is not None
     assert d["d2d_copy"]["bytes"] == 2 * 2 * 4 * d["config"]["chunk_elems"]
