@@ -195,9 +195,10 @@ def time_launches(calls, reps, stream, labels=None, label=None, warm=3):
     return per, ev[0].elapsed_time(ev[reps]) / reps
 
 
-def kernel_leg(plan, wl, rank, reps, dev, stream, labels=None):
-    """Each of the four calls ``reps`` times over rotating input/output sets
-    of more than ROTATE_BYTES in total; per kernel: event statistics."""
+def kernel_leg(plan, wl, rank, reps, dev, stream, labels=None, kernels=KERNELS, tag=""):
+    """Each of ``kernels`` ``reps`` times over rotating input/output sets of
+    more than ROTATE_BYTES in total; per kernel: event statistics.  Launches
+    are labelled name + tag."""
     import torch
 
     W, S, E = plan.world_size, plan.chunk_elems, wl.total_elems
@@ -206,11 +207,11 @@ def kernel_leg(plan, wl, rank, reps, dev, stream, labels=None):
     gen = torch.Generator(device=dev)
     gen.manual_seed(2000 + wl.key)
     res = {}
-    for name in KERNELS:
+    for name in kernels:
         nsets = min(64, max(2, -(-ROTATE_BYTES // abytes[name])))
         sets = [kernel_set(name, plan, wl, rank, dev, gen) for _ in range(nsets)]
         torch.cuda.synchronize()
-        per, b2b = time_launches([c for c, _ in sets], reps, stream, labels, name, warm=min(nsets, 8))
+        per, b2b = time_launches([c for c, _ in sets], reps, stream, labels, name + tag, warm=min(nsets, 8))
         res[name] = {"reps": reps, "sets": nsets, "set_bytes": abytes[name], **{
             "event_" + k: v for k, v in stats_us(per).items()}, "b2b_avg_us": round(b2b * 1e3, 3)}
         del sets
@@ -410,12 +411,184 @@ def child_main(spec_path, out_path):
         if spec.get("ceilings"):
             out["ceilings"] = ceiling_leg(plan, spec["rank"], spec["reps"], dev, stream, labels)
         plan.close()
+    elif spec["mode"] == "records":
+        wl = workload(spec["workload"])
+        plan = BucketPlan(wl.world_size, wl.dims)
+        for r in spec["ranks"]:
+            kernel_leg(plan, wl, r, spec["reps"], dev, stream, labels, record_kernels(r), f"@{r}")
+        plan.close()
     elif spec["mode"] == "pack_sweep":
         out["cases"] = pack_sweep_leg(spec["reps"], dev, stream, labels)
     out["labels"] = labels
     with open(out_path, "w") as f:
         json.dump(out, f)
     return 0
+
+
+# ----------------------------------------------------------------- result records
+
+RECORD_WORKLOADS = (1, 2, 3, 4, 5, 6, 7)
+
+
+def record_kernels(rank):
+    """The calls recorded at a rank: all four at rank 0; at the other ranks
+    the two whose work depends on the rank (the unpack and rs_pack read and
+    write the whole block at every rank)."""
+    return KERNELS if rank == 0 else ("ag_pack", "rs_reduce")
+
+
+def oracle_inputs(name, wl, plan, rank):
+    """The oracle's inputs of one call (random bit patterns, finite where the
+    call computes with them), as the CPU-baseline leg draws them."""
+    import numpy as np
+
+    import oracle.fsdp_oracle as O
+    from synth import random_bits16, random_bits32
+
+    W, S = plan.world_size, plan.chunk
+    if name == "ag_pack":
+        shards = [random_bits32([1, p], O.local_elems(plan, p, rank)).view(np.float32) for p in range(len(wl.dims))]
+        return [np.where(np.isfinite(s), s, np.float32(0)) for s in shards]
+    if name == "ag_unpack":
+        return random_bits16([2], W * S)
+    if name == "rs_pack":
+        return [random_bits16([3, p], n * k).reshape(n, k) for p, (n, k) in enumerate(wl.dims)]
+    return random_bits16([4], W * S) & np.uint16(0xBFFF)
+
+
+def oracle_call(name, plan, rank, x):
+    import oracle.fsdp_oracle as O
+
+    if name == "ag_pack":
+        return O.ag_pack(plan, rank, x)
+    if name == "ag_unpack":
+        return O.ag_unpack(plan, x)
+    if name == "rs_pack":
+        return O.rs_pack(plan, x)
+    return O.rs_reduce(plan, rank, x)
+
+
+def library_matches(name, gpu_plan, rank, x, want):
+    """One library call on the oracle's inputs: is every output bit equal?"""
+    import numpy as np
+    import torch
+
+    dev = torch.device("cuda:0")
+
+    def up16(a):
+        return torch.from_numpy(np.ascontiguousarray(a).reshape(-1).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    def down(t, dtype):
+        return t.view(torch.int16 if dtype == np.uint16 else torch.int32).cpu().numpy().view(dtype)
+
+    P, S, W = gpu_plan.num_params, gpu_plan.chunk_elems, gpu_plan.world_size
+    if name == "ag_pack":
+        shards = [torch.from_numpy(np.ascontiguousarray(a)).to(dev) for a in x]
+        out = torch.empty(S, dtype=torch.bfloat16, device=dev)
+        gpu_plan.ag_pack(rank, shards, out)
+        ok = bool(np.array_equal(down(out, np.uint16), want))
+    elif name == "ag_unpack":
+        params = [torch.empty(gpu_plan.full_elems(p), dtype=torch.bfloat16, device=dev) for p in range(P)]
+        gpu_plan.ag_unpack(up16(x), params)
+        ok = all(np.array_equal(down(params[p], np.uint16), want[p].reshape(-1)) for p in range(P))
+    elif name == "rs_pack":
+        send = torch.empty(W * S, dtype=torch.bfloat16, device=dev)
+        gpu_plan.rs_pack([up16(g) for g in x], send)
+        ok = bool(np.array_equal(down(send, np.uint16), want))
+    else:
+        outs = [torch.empty(gpu_plan.local_elems(p, rank), dtype=torch.float32, device=dev) for p in range(P)]
+        gpu_plan.rs_reduce(rank, up16(x), outs)
+        ok = all(np.array_equal(down(outs[p], np.uint32), want[p].reshape(-1).view(np.uint32)) for p in range(P))
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return ok
+
+
+def records_main(out_dir, reps, keys=RECORD_WORKLOADS):
+    """One record per (workload, kernel, rank): kernel-trace and event
+    statistics of the per-kernel leg, GB/s and share of peak, committed
+    counter bytes where they match the source, the oracle's time for the
+    same call on the host, and whether the library's output equals the
+    oracle's bit for bit on the oracle's inputs (full size)."""
+    import torch
+
+    import oracle.fsdp_oracle as O
+    from paper_2411_00284_amd import BucketPlan
+    from synth import workload
+
+    os.makedirs(out_dir, exist_ok=True)
+    cores = len(os.sched_getaffinity(0))
+    records = []
+    for key in keys:
+        wl = workload(key)
+        W = wl.world_size
+        ranks = sorted({0, W // 2, W - 1})
+        print(f"[records] {wl.name}: traced leg", file=sys.stderr, flush=True)
+        child, per, names = traced_child({"mode": "records", "workload": key, "ranks": ranks, "reps": reps})
+        dev = torch.device("cuda:0")
+        torch.cuda.set_device(dev)
+        stream = torch.cuda.current_stream()
+        plan = BucketPlan(W, wl.dims)
+        oplan = O.make_plan(W, wl.dims, 8)
+        S, E = plan.chunk_elems, wl.total_elems
+        for r in ranks:
+            print(f"[records] {wl.name}: rank {r}", file=sys.stderr, flush=True)
+            leg = kernel_leg(plan, wl, r, reps, dev, stream, kernels=record_kernels(r))
+            V = sum(plan.local_elems(p, r) for p in range(plan.num_params))
+            abytes = algorithmic_bytes(W, S, E, V)
+            for name in record_kernels(r):
+                x = oracle_inputs(name, wl, oplan, r)
+                t0 = time.perf_counter()
+                want = oracle_call(name, oplan, r, x)
+                oracle_s = time.perf_counter() - t0
+                parity = library_matches(name, plan, r, x, want)
+                del x, want
+                lab = f"{name}@{r}"
+                tr = stats_us(per[lab][-reps:]) if child is not None and lab in per else None
+                us = tr["median_us"] if tr else leg[name]["event_median_us"]
+                traffic = read_traffic(name, wl.name) if r == 0 else None
+                records.append({
+                    "workload": wl.name, "config": key, "world_size": W, "rank": r if name in ("ag_pack", "rs_reduce") else None,
+                    "kernel": name, "symbol": names[lab] if tr else kernel_symbol(name, plan, r, cus_of(dev)),
+                    "bytes": abytes[name], "reps": reps, "sets": leg[name]["sets"],
+                    "event_median_us": leg[name]["event_median_us"], "event_min_us": leg[name]["event_min_us"],
+                    "rocprof_median_us": tr["median_us"] if tr else None, "rocprof_min_us": tr["min_us"] if tr else None,
+                    "GBps": round(abytes[name] / (us * 1e-6) / 1e9, 1),
+                    "frac": round(abytes[name] / (us * 1e-6) / 1e9 / PEAK_GBPS, 4),
+                    "counter_bytes": traffic, "counter_ratio": None if traffic is None else round(traffic / abytes[name], 4),
+                    "oracle_s": round(oracle_s, 3), "oracle_threads": 1, "host_cores": cores,
+                    "oracle_GBps": round(abytes[name] / oracle_s / 1e9, 3), "parity": parity,
+                    "kernel_source_sha256": kernel_source_sha(),
+                })
+        plan.close()
+        torch.cuda.empty_cache()
+    with open(os.path.join(out_dir, "records.jsonl"), "w") as f:
+        for rec in records:
+            f.write(json.dumps(rec) + "\n")
+    with open(os.path.join(out_dir, "records.md"), "w") as f:
+        f.write(records_table(records))
+    print(json.dumps({"records": len(records), "dir": out_dir,
+                      "parity": all(r["parity"] for r in records)}), flush=True)
+    return 0 if all(r["parity"] for r in records) else 1
+
+
+def cus_of(dev):
+    import torch
+    return torch.cuda.get_device_properties(dev).multi_processor_count
+
+
+def records_table(records):
+    lines = ["| workload | W | rank | kernel | algorithmic bytes | trace median us | trace min us | GB/s | % of peak "
+             "| event median us | counter / alg | oracle s (1 thread) | bit-exact |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in records:
+        lines.append("| {workload} | {world_size} | {rk} | {kernel} | {bytes} | {tm} | {tn} | {GBps} | {pct:.1f} | "
+                     "{event_median_us} | {cr} | {oracle_s} | {par} |".format(
+                         **r, rk="all" if r["rank"] is None else r["rank"], tm=r["rocprof_median_us"],
+                         tn=r["rocprof_min_us"], pct=100 * r["frac"],
+                         cr="" if r["counter_ratio"] is None else r["counter_ratio"],
+                         par="yes" if r["parity"] else "NO"))
+    return "\n".join(lines) + "\n"
 
 
 # ----------------------------------------------------------------- ag_pack over bucket sizes
@@ -516,11 +689,18 @@ def main(argv=None):
                     help="also time the step replayed from a HIP graph")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the steps, run a plain 1 GiB device copy (for counter scaling)")
+    ap.add_argument("--records", metavar="DIR",
+                    help="instead of the steps: one record per (workload, kernel, rank) for workloads 1-7, "
+                         "written to DIR/records.jsonl and DIR/records.md")
+    ap.add_argument("--record-workloads", type=int, nargs="+", default=list(RECORD_WORKLOADS),
+                    help="the workloads --records covers (default: all seven)")
     ap.add_argument("--child", nargs=2, metavar=("SPEC", "OUT"), help=argparse.SUPPRESS)
     args = ap.parse_args(argv)
 
     if args.child:
         return child_main(*args.child)
+    if args.records:
+        return records_main(args.records, max(1, args.kernel_reps), tuple(args.record_workloads))
     if args.gpus != 1:
         print(f"bench.py: one GPU only (asked for --gpus {args.gpus}); "
               "the path has no collective and runs per rank", file=sys.stderr)
@@ -558,18 +738,6 @@ def main(argv=None):
     E = wl.total_elems
     V0 = sum(plan.local_elems(p, rank) for p in range(P))
     stream = torch.cuda.current_stream()
-
-    # ---- the per-kernel leg: each call over rotating sets of > 1.5 GiB
-    leg = kernel_leg(plan, wl, rank, reps, dev, stream)
-    ceilings = None
-    if args.ceilings:
-        ceilings = ceiling_leg(plan, rank, reps, dev, stream)
-        for name, c in ceilings.items():
-            tr = trace.get(name) if trace and "error" not in trace else None
-            us = tr["rocprof_median_us"] if tr else c["event_median_us"]
-            c["trace"] = tr
-            c["GBps"] = round(c["bytes"] / (us * 1e-6) / 1e9, 1)
-            c["frac"] = round(c["bytes"] / (us * 1e-6) / 1e9 / PEAK_GBPS, 4)
 
     # ---- seeded synthetic inputs, resident in HBM before timing
     g = torch.Generator(device=dev)
@@ -628,6 +796,19 @@ def main(argv=None):
         run_step(events[k])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+
+    # ---- the per-kernel leg (after the steps, so that its allocations do not
+    # precede the step buffers): each call over rotating sets of > 1.5 GiB
+    leg = kernel_leg(plan, wl, rank, reps, dev, stream)
+    ceilings = None
+    if args.ceilings:
+        ceilings = ceiling_leg(plan, rank, reps, dev, stream)
+        for name, c in ceilings.items():
+            tr = trace.get(name) if trace and "error" not in trace else None
+            us = tr["rocprof_median_us"] if tr else c["event_median_us"]
+            c["trace"] = tr
+            c["GBps"] = round(c["bytes"] / (us * 1e-6) / 1e9, 1)
+            c["frac"] = round(c["bytes"] / (us * 1e-6) / 1e9 / PEAK_GBPS, 4)
 
     per_kernel_ms = {name: [] for name in KERNELS}
     for ev in events:

@@ -109,11 +109,12 @@ __device__ __forceinline__ void add8(float (&a)[8], const u32x4& x, bool init) {
 // Outputs [0, n) (n a multiple of the tile, kRBlock * 8 * kRSteps): source i
 // of output k at src[i * stride + k].  A workgroup owns one tile; each thread
 // 8 consecutive outputs of each of kRSteps rows.  Loads of kBatch sources are
-// issued before their adds, which run in rank order.  With `store`, the
+// issued before their adds, which run in rank order.  With kStore, the
 // averages go through LDS so that every store instruction of a wave writes
-// one contiguous run.
+// one contiguous run; without, nothing is stored.
+template <bool kStore>
 __global__ void __launch_bounds__(kRBlock) probe_reduce_kernel(const uint16_t* __restrict__ src, int64_t stride,
-                                                                 int W, float* __restrict__ dst, int store,
+                                                                 int W, float* __restrict__ dst,
                                                                  uint32_t* __restrict__ sink) {
     constexpr int kRow = kRBlock * 8;
     const int t = threadIdx.x;
@@ -135,7 +136,7 @@ __global__ void __launch_bounds__(kRBlock) probe_reduce_kernel(const uint16_t* _
                 for (int u = 0; u < kRSteps; ++u) add8(acc[u], x[b][u], i0 + b == 0);
     }
     const float wf = float(W);
-    if (!store) {
+    if constexpr (!kStore) {
         uint32_t h = 0;
 #pragma unroll
         for (int u = 0; u < kRSteps; ++u)
@@ -208,6 +209,9 @@ extern "C" int probe_strided_reduce(const uint16_t* src, int64_t stride, int32_t
     if (n <= 0 || n % kTile || W < 1 || stride < n || stride % 8 || !src || !dst || !sink ||
         (uintptr_t(src) & 15) || (uintptr_t(dst) & 15) || !grid_ok(n / kTile))
         return hipErrorInvalidValue;
-    probe_reduce_kernel<<<dim3(unsigned(n / kTile)), dim3(kRBlock), 0, stream>>>(src, stride, W, dst, store, sink);
+    if (store)
+        probe_reduce_kernel<true><<<dim3(unsigned(n / kTile)), dim3(kRBlock), 0, stream>>>(src, stride, W, dst, sink);
+    else
+        probe_reduce_kernel<false><<<dim3(unsigned(n / kTile)), dim3(kRBlock), 0, stream>>>(src, stride, W, dst, sink);
     return hipGetLastError();
 }

@@ -55,3 +55,23 @@ def test_bench_line_on_the_toy_block():
             assert k["timing"].startswith("rocprofv3")
     assert d["kernel_trace"] is not None
     assert d["d2d_copy"]["bytes"] == 2 * 2 * 4 * d["config"]["chunk_elems"]
+
+
+def test_records_on_the_toy_block(tmp_path):
+    """--records: one record per (workload, kernel, rank), every one bit-exact
+    against the oracle and carrying the per-kernel leg's statistics."""
+    print("bench.py --records (toy block)", flush=True)
+    res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--records", str(tmp_path),
+                          "--record-workloads", "1"], capture_output=True, text=True, timeout=240)
+    assert res.returncode == 0, res.stderr[-2000:]
+    recs = [json.loads(l) for l in open(tmp_path / "records.jsonl")]
+    # ranks 0, 2 and 3 of W = 4: four calls at rank 0, the two per-rank calls at the others
+    assert len(recs) == 8
+    assert sorted((r["kernel"], r["rank"]) for r in recs) == sorted(
+        [("ag_pack", 0), ("ag_pack", 2), ("ag_pack", 3), ("rs_reduce", 0), ("rs_reduce", 2), ("rs_reduce", 3),
+         ("ag_unpack", None), ("rs_pack", None)])
+    for r in recs:
+        assert r["parity"] is True and r["reps"] >= 30 and r["bytes"] > 0
+        assert r["rocprof_median_us"] is None or r["rocprof_median_us"] > 0
+        assert 0 < r["frac"] and r["oracle_threads"] == 1
+    assert (tmp_path / "records.md").read_text().count("| yes |") == 8
