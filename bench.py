@@ -47,14 +47,17 @@ KERNELS = ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")
 # Device symbols of the kernels each call launches (bf16 wire, one contiguous
 # buffer), as rocprofv3 prints them; a kernel trace taken during the run
 # replaces these with the names it saw.  A rank shard of fewer than 4
-# full-size reduce tiles per CU is reduced with 128-thread workgroups.
+# full-size reduce tiles per CU is reduced with 128-thread workgroups; a
+# single-chunk pack of fewer than 4 big (256-thread, 2-step) tiles per CU
+# packs with 128-thread, 1-step tiles.
 KERNEL_SYMBOLS = {
-    "ag_pack": "ag_pack_kernel<1, OneChunk>",
+    "ag_pack": "ag_pack_kernel<1, OneChunk, 256, 2>",
     "ag_unpack": "ag_unpack_kernel<ContigChunks>",
     "rs_pack": "rs_pack_kernel<ContigChunks, 0>",
     "rs_reduce": "rs_reduce_kernel<ContigChunks, unsigned short, 256>",
 }
 REDUCE_SMALL_SYMBOL = "rs_reduce_kernel<ContigChunks, unsigned short, 128>"
+PACK_SMALL_SYMBOL = "ag_pack_kernel<1, OneChunk, 128, 1>"
 KERNEL_BASENAMES = ("ag_pack_kernel", "ag_unpack_kernel", "rs_pack_kernel", "rs_reduce_kernel", "probe_read_kernel",
                     "probe_fill_kernel", "probe_copy_kernel", "probe_cast_kernel", "probe_reduce_kernel")
 PROBES_LIB = os.path.join(ROOT, "paper_2411_00284_amd", "libfsdp_probes.so")
@@ -65,9 +68,12 @@ PROFILES = os.path.join(ROOT, "profiles")
 # the 256 MB Infinity Cache.
 ROTATE_BYTES = 3 << 29
 SLEEP_CYCLES = 50_000_000                # a device-side wait that lets the host enqueue a whole leg
-# The full-size reduce tile and the small-shard threshold of the library.
+# The full-size reduce tile, the big pack tile and the thresholds of the
+# library's choice between the two shapes of each.
 REDUCE_TILE = 256 * 8 * 2
 SMALL_SHARD_TILES_PER_CU = 4
+PACK_BIG_TILE = 256 * 8 * 2
+PACK_BIG_TILES_PER_CU = 4
 
 
 def algorithmic_bytes(W, S, E, V0):
@@ -86,6 +92,11 @@ def kernel_symbol(name, plan, rank, cus):
         full_tiles = sum(-(-plan.local_elems(p, rank) // REDUCE_TILE) for p in range(plan.num_params))
         if full_tiles < SMALL_SHARD_TILES_PER_CU * cus:
             return REDUCE_SMALL_SYMBOL
+    if name == "ag_pack":
+        ends = [plan.offset(p + 1) for p in range(plan.num_params - 1)] + [plan.chunk_elems]
+        big = sum(-(-(e - plan.offset(p)) // PACK_BIG_TILE) for p, e in enumerate(ends))
+        if big < PACK_BIG_TILES_PER_CU * cus:
+            return PACK_SMALL_SYMBOL
     return KERNEL_SYMBOLS[name]
 
 
@@ -339,6 +350,15 @@ def rocprof_path():
 
 
 def traced_child(spec, timeout=600):
+    spec = dict(spec)
+    from paper_2411_00284_amd import _native
+    if os.path.abspath(_native.LIB_PATH) != os.path.abspath(os.path.join(ROOT, "paper_2411_00284_amd",
+                                                                         "libfsdp_bucket.so")):
+        spec["library"] = _native.LIB_PATH
+    return _traced_child(spec, timeout)
+
+
+def _traced_child(spec, timeout):
     """Run ``bench.py --child`` with ``spec`` as a child process under
     ``rocprofv3 --kernel-trace`` and return (child result, per-launch kernel
     durations in ms grouped by the child's labels, kernel names per label), or
@@ -391,14 +411,26 @@ def traced_child(spec, timeout=600):
         shutil.rmtree(tmp, ignore_errors=True)
 
 
+def use_library(path):
+    """Point the binding at another build of the library (before it loads)."""
+    from paper_2411_00284_amd import _native
+
+    if _native._lib is not None:
+        raise RuntimeError("the library is already loaded")
+    _native.LIB_PATH = os.path.abspath(path)
+
+
 def child_main(spec_path, out_path):
     """The traced child: runs the leg the spec names and writes its labels."""
     import torch
 
+    spec = json.load(open(spec_path))
+    if spec.get("library"):
+        use_library(spec["library"])
+
     from paper_2411_00284_amd import BucketPlan
     from synth import workload
 
-    spec = json.load(open(spec_path))
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
@@ -694,9 +726,14 @@ def main(argv=None):
                          "written to DIR/records.jsonl and DIR/records.md")
     ap.add_argument("--record-workloads", type=int, nargs="+", default=list(RECORD_WORKLOADS),
                     help="the workloads --records covers (default: all seven)")
+    ap.add_argument("--library", metavar="SO",
+                    help="load this build of libfsdp_bucket.so (a launch-shape variant made with "
+                         "`python -m paper_2411_00284_amd.build -DNAME=VALUE --out DIR`) instead of the package's")
     ap.add_argument("--child", nargs=2, metavar=("SPEC", "OUT"), help=argparse.SUPPRESS)
     args = ap.parse_args(argv)
 
+    if args.library:
+        use_library(args.library)
     if args.child:
         return child_main(*args.child)
     if args.records:

@@ -6,6 +6,10 @@ packed-fp32 target feature turned off, so the compiler emits only scalar fp32
 adds and the correctly rounded fp32 division sequence.
 
 Usage: ``python -m paper_2411_00284_amd.build`` (or ``build()`` from Python).
+``-DNAME=VALUE`` overrides a tuning macro (``FSDP_PACK_BLOCK``,
+``FSDP_BLOCKS_PER_CU``, ...) and ``--out DIR`` writes that variant's library
+to DIR instead of the package (the benchmark's ``--library`` loads it), for
+measuring launch shapes; results never depend on them.
 """
 
 from __future__ import annotations
@@ -49,20 +53,28 @@ def _run(cmd, verbose):
     return res
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link the library; returns its path."""
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose: bool = False, defines=(), out_dir: str | None = None) -> str:
+    """Compile every source and link the library; returns its path.  With
+    ``defines`` (``NAME=VALUE`` macro overrides) or ``out_dir``, only the
+    bucket library is built, into ``out_dir``."""
+    variant = bool(defines) or out_dir is not None
+    bdir = os.path.join(out_dir, "_build") if out_dir else BUILD
+    lib_path = os.path.join(out_dir, LIB_NAME) if out_dir else LIB_PATH
+    os.makedirs(bdir, exist_ok=True)
     inc = [f"-I{INCLUDE}", f"-I{CSRC}", f"-I{os.path.join(ROCM, 'include')}"]
-    kobj = os.path.join(BUILD, "bucket_kernels.o")
-    _run([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, "bucket_kernels.hip"), "-o", kobj], verbose)
+    dflags = [f"-D{d}" for d in defines]
+    kobj = os.path.join(bdir, "bucket_kernels.o")
+    _run([HIPCC, *DEVICE_FLAGS, *dflags, *inc, "-c", os.path.join(CSRC, "bucket_kernels.hip"), "-o", kobj], verbose)
     hobjs = []
     for src in HOST_SOURCES:
-        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-        _run(["g++", *HOST_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
+        obj = os.path.join(bdir, os.path.splitext(src)[0] + ".o")
+        _run(["g++", *HOST_FLAGS, *dflags, *inc, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
         hobjs.append(obj)
-    tmp = LIB_PATH + f".tmp{os.getpid()}"
+    tmp = lib_path + f".tmp{os.getpid()}"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, kobj, *hobjs], verbose)
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, lib_path)
+    if variant:
+        return lib_path
     pobj = os.path.join(BUILD, "ceiling_probes.o")
     _run([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, "ceiling_probes.hip"), "-o", pobj], verbose)
     tmp = PROBES_PATH + f".tmp{os.getpid()}"
@@ -76,4 +88,7 @@ def clean() -> None:
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    args = sys.argv[1:]
+    defs = [a[2:] for a in args if a.startswith("-D")]
+    out = args[args.index("--out") + 1] if "--out" in args else None
+    print(build(verbose="-v" in args, defines=defs, out_dir=out))

@@ -314,19 +314,20 @@ __device__ __forceinline__ uint2 cast4(float4 a) {
 // written to every destination.  Each thread handles 4 elements per sub-step
 // (16 bytes of fp32 in), so every load and store instruction of a wave covers
 // one contiguous run; the full tiles of a 16-bit push take 8 per thread.
-template <int kOut, class Dst, bool kNt = true>
+template <int kOut, class Dst, bool kNt = true, int kB = kPackBlock, int kS = kPackSteps>
 __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt) {
+    constexpr int64_t kTile = int64_t(kB) * kVec * kS;
     constexpr bool kCast = kOut != kF32;
     typedef typename std::conditional<kCast, uint16_t, uint32_t>::type Out;
-    constexpr int kSub = 2 * kPackSteps;
+    constexpr int kSub = 2 * kS;
     constexpr bool kOne = std::is_same<Dst, OneChunk>::value;
     const int ndst = kOne ? 1 : a.ndst;
     const int64_t off = a.off[p];
     const int64_t region = a.off[p + 1] - off;
     const int64_t valid = a.valid[p];
     const float* __restrict__ src = a.src[p];
-    const int64_t lo = int64_t(lt) * kPackTile;
-    const int64_t hi = min(lo + kPackTile, region);
+    const int64_t lo = int64_t(lt) * kTile;
+    const int64_t hi = min(lo + kTile, region);
     if (lo >= hi) return;
     // every destination chunk is 16-byte aligned, so one test covers them all
     const bool vec = is_aligned16(src) && is_aligned16(reinterpret_cast<Out*>(a.dst.at(0)) + off);
@@ -334,11 +335,11 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
         // Pushed to W destinations, the stores outnumber the loads W to 1:
         // each thread casts 8 consecutive elements and writes them with one
         // 16-byte store per destination.
-        if (vec && hi - lo == kPackTile && lo + kPackTile <= valid) {
-            uint4 y[kPackSteps];
+        if (vec && hi - lo == kTile && lo + kTile <= valid) {
+            uint4 y[kS];
 #pragma unroll
-            for (int u = 0; u < kPackSteps; ++u) {
-                const float* s8 = src + lo + (int64_t(u) * kPackBlock + threadIdx.x) * 8;
+            for (int u = 0; u < kS; ++u) {
+                const float* s8 = src + lo + (int64_t(u) * kB + threadIdx.x) * 8;
                 const uint2 c0 = cast4<kOut>(ld16f(s8));
                 const uint2 c1 = cast4<kOut>(ld16f(s8 + 4));
                 y[u] = make_uint4(c0.x, c0.y, c1.x, c1.y);
@@ -346,20 +347,20 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
             for (int j = 0; j < ndst; ++j) {
                 Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
 #pragma unroll
-                for (int u = 0; u < kPackSteps; ++u) st16<kNt>(dst + lo + (int64_t(u) * kPackBlock + threadIdx.x) * 8, y[u]);
+                for (int u = 0; u < kS; ++u) st16<kNt>(dst + lo + (int64_t(u) * kB + threadIdx.x) * 8, y[u]);
             }
             return;
         }
     }
-    if (vec && hi - lo == kPackTile && lo + kPackTile <= valid) {
+    if (vec && hi - lo == kTile && lo + kTile <= valid) {
         float4 x[kSub];
 #pragma unroll
-        for (int u = 0; u < kSub; ++u) x[u] = ld16f(src + lo + (int64_t(u) * kPackBlock + threadIdx.x) * 4);
+        for (int u = 0; u < kSub; ++u) x[u] = ld16f(src + lo + (int64_t(u) * kB + threadIdx.x) * 4);
         for (int j = 0; j < ndst; ++j) {
             Out* __restrict__ dst = reinterpret_cast<Out*>(a.dst.at(j)) + off;
 #pragma unroll
             for (int u = 0; u < kSub; ++u) {
-                const int64_t g = lo + (int64_t(u) * kPackBlock + threadIdx.x) * 4;
+                const int64_t g = lo + (int64_t(u) * kB + threadIdx.x) * 4;
                 if (kCast) st8<kNt>(dst + g, cast4<kOut>(x[u]));
                 else st16f<kNt>(reinterpret_cast<float*>(dst + g), x[u]);
             }
@@ -367,7 +368,7 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
         return;
     }
     for (int u = 0; u < kSub; ++u) {
-        const int64_t g = lo + (int64_t(u) * kPackBlock + threadIdx.x) * 4;
+        const int64_t g = lo + (int64_t(u) * kB + threadIdx.x) * 4;
         if (g >= hi) break;
         if (vec && g + 4 <= hi && (g + 4 <= valid || g >= valid)) {
             const float4 x = g < valid ? ld16f(src + g) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -394,15 +395,16 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
 // chain is kept short: tile_start holds INT_MAX past the last parameter (no
 // wait for the parameter count before the table load), the grid never exceeds
 // the tile count (the first tile needs no bound check), and a tile's first
-// index comes from the looked-up lane rather than another table load.
-template <int kOut, class Dst>
-__global__ void __launch_bounds__(kPackBlock) ag_pack_kernel(const PackArgs<Dst> a) {
+// index comes from the looked-up lane rather than another table load.  A
+// tile is kB threads x kS steps of 8 elements.
+template <int kOut, class Dst, int kB, int kS>
+__global__ void __launch_bounds__(kB) ag_pack_kernel(const PackArgs<Dst> a) {
     const int my_start = a.tile_start[threadIdx.x & 63];
     int64_t step = blockIdx.x;
     do {
         const int t = int(step);
         const int p = param_of_tile(my_start, t);
-        pack_tile<kOut>(a, p, t - __builtin_amdgcn_readlane(my_start, p));
+        pack_tile<kOut, Dst, true, kB, kS>(a, p, t - __builtin_amdgcn_readlane(my_start, p));
         step += gridDim.x;
     } while (step < a.ntiles);
 }
@@ -876,6 +878,8 @@ __global__ void __launch_bounds__(kB) rs_reduce_kernel(const ReduceArgs<Chunks> 
 
 // Below this many full-size reduce tiles per CU, the reduce uses half-size tiles.
 constexpr int kSmallShardTilesPerCU = 4;
+// From this many big pack tiles per CU up, a single-chunk pack uses them.
+constexpr int kPackBigTilesPerCU = 4;
 
 int cu_count(fsdp_status* st) {
     static std::atomic<int> cache[64];
@@ -1005,25 +1009,50 @@ fsdp_status do_ag_pack(const Plan& pl, int32_t rank, const float* const* shards,
     if (shards == nullptr) return fail(FSDP_ERR_INVALID, "shards is NULL");
     PackArgs<Dst> a{};
     Spans ins;
-    int64_t nt = 0;   // at most the planner's checked pack tile count
+    int64_t nt = 0, nt_big = 0;   // at most the planner's checked pack tile count
     for (int p = 0; p < pl.nparams; ++p) {
         const int64_t v = pl.local_elems(p, rank);
         if ((st = check_param_ptr(shards[p], v, 4, p, "shards")) != FSDP_OK) return st;
         a.src[p] = shards[p];
         a.off[p] = pl.off[p];
         a.valid[p] = v;
-        a.tile_start[p] = int32_t(nt);
         nt += tiles(pl.off[p + 1] - pl.off[p], kPackTile);
+        nt_big += tiles(pl.off[p + 1] - pl.off[p], kPackBigTile);
         if (v > 0) ins.add(shards[p], v * 4);
     }
     a.off[pl.nparams] = pl.chunk;
-    for (int p = pl.nparams; p < PMAX; ++p) a.tile_start[p] = INT32_MAX;   // never a tile's parameter
     a.dst = dst;
     a.ndst = ndst;
     a.nparams = pl.nparams;
     if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
-    a.ntiles = int32_t(nt);
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
+    // A single-chunk pack of at least kPackBigTilesPerCU big tiles per CU
+    // takes the big tiles (more bytes in flight per wave); smaller buckets keep
+    // the small ones, which spread evenly over the CUs.  (The first HIP call:
+    // every argument is checked.)
+    bool big = false;
+    if constexpr (std::is_same<Dst, OneChunk>::value) {
+        if (!cached) {
+            const int cus = cu_count(&st);
+            if (st != FSDP_OK) return st;
+            big = nt_big >= int64_t(kPackBigTilesPerCU) * cus;
+        }
+    }
+    const int64_t tile = big ? kPackBigTile : kPackTile;
+    int64_t t0 = 0;
+    for (int p = 0; p < pl.nparams; ++p) {
+        a.tile_start[p] = int32_t(t0);
+        t0 += tiles(pl.off[p + 1] - pl.off[p], tile);
+    }
+    for (int p = pl.nparams; p < PMAX; ++p) a.tile_start[p] = INT32_MAX;   // never a tile's parameter
+    a.ntiles = int32_t(t0);
+    if (big) {
+        if (wire == FSDP_DTYPE_BF16)
+            return launch(pl, ag_pack_kernel<kBF16, Dst, kPackBigBlock, kPackBigSteps>, a, a.ntiles, kPackBigBlock, stream);
+        if (wire == FSDP_DTYPE_F16)
+            return launch(pl, ag_pack_kernel<kF16, Dst, kPackBigBlock, kPackBigSteps>, a, a.ntiles, kPackBigBlock, stream);
+        return launch(pl, ag_pack_kernel<kF32, Dst, kPackBigBlock, kPackBigSteps>, a, a.ntiles, kPackBigBlock, stream);
+    }
     if constexpr (std::is_same<Dst, OneChunk>::value) {
         if (cached) {
             if (wire == FSDP_DTYPE_BF16) return launch(pl, push_pack_kernel<kBF16>, a, a.ntiles, kPackBlock, stream);
@@ -1031,9 +1060,11 @@ fsdp_status do_ag_pack(const Plan& pl, int32_t rank, const float* const* shards,
             return launch(pl, push_pack_kernel<kF32>, a, a.ntiles, kPackBlock, stream);
         }
     }
-    if (wire == FSDP_DTYPE_BF16) return launch(pl, ag_pack_kernel<kBF16, Dst>, a, a.ntiles, kPackBlock, stream);
-    if (wire == FSDP_DTYPE_F16) return launch(pl, ag_pack_kernel<kF16, Dst>, a, a.ntiles, kPackBlock, stream);
-    return launch(pl, ag_pack_kernel<kF32, Dst>, a, a.ntiles, kPackBlock, stream);
+    if (wire == FSDP_DTYPE_BF16)
+        return launch(pl, ag_pack_kernel<kBF16, Dst, kPackBlock, kPackSteps>, a, a.ntiles, kPackBlock, stream);
+    if (wire == FSDP_DTYPE_F16)
+        return launch(pl, ag_pack_kernel<kF16, Dst, kPackBlock, kPackSteps>, a, a.ntiles, kPackBlock, stream);
+    return launch(pl, ag_pack_kernel<kF32, Dst, kPackBlock, kPackSteps>, a, a.ntiles, kPackBlock, stream);
 }
 
 fsdp_status do_ag_pack_one(const fsdp_plan* h, int32_t rank, const float* const* shards, fsdp_dtype wire,

@@ -12,7 +12,8 @@ namespace fsdp {
 // Work tiles.  The copy kernels (ag_unpack, rs_pack) run kCopyBlock threads
 // that move 8 elements (16 bytes of bf16) per thread and step, kCopySteps
 // steps per tile; ag_pack runs kPackBlock threads that cast 8 elements per
-// thread and step, kPackSteps steps per tile; the reduction runs kReduceBlock
+// thread and step, kPackSteps steps per tile (kPackBigBlock and kPackBigSteps
+// for a large single-chunk pack); the reduction runs kReduceBlock
 // threads that each own kReduceSteps groups of 8 outputs.  One tile per
 // workgroup (small tiles, many workgroups) measured fastest for these HBM
 // streams.
@@ -27,6 +28,12 @@ namespace fsdp {
 #endif
 #ifndef FSDP_PACK_BLOCK
 #define FSDP_PACK_BLOCK 128
+#endif
+#ifndef FSDP_PACK_BIG_BLOCK
+#define FSDP_PACK_BIG_BLOCK 256
+#endif
+#ifndef FSDP_PACK_BIG_STEPS
+#define FSDP_PACK_BIG_STEPS 2
 #endif
 #ifndef FSDP_REDUCE_BLOCK
 #define FSDP_REDUCE_BLOCK 256
@@ -44,6 +51,10 @@ constexpr int64_t kWidenTile = int64_t(kCopyBlock) * 4 * kCopySteps;
 constexpr int kPackBlock = FSDP_PACK_BLOCK;
 constexpr int kPackSteps = FSDP_PACK_STEPS;
 constexpr int64_t kPackTile = int64_t(kPackBlock) * kVec * kPackSteps;
+// The single-chunk pack of a large bucket uses bigger tiles.
+constexpr int kPackBigBlock = FSDP_PACK_BIG_BLOCK;
+constexpr int kPackBigSteps = FSDP_PACK_BIG_STEPS;
+constexpr int64_t kPackBigTile = int64_t(kPackBigBlock) * kVec * kPackBigSteps;
 constexpr int kReduceBlock = FSDP_REDUCE_BLOCK;
 constexpr int kReduceSteps = FSDP_REDUCE_STEPS;
 constexpr int64_t kReduceTile = int64_t(kReduceBlock) * kVec * kReduceSteps;
