@@ -48,10 +48,10 @@ KERNELS = ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")
 # buffer), as rocprofv3 prints them; a kernel trace taken during the run
 # replaces these with the names it saw.  A rank shard of fewer than 4
 # full-size reduce tiles per CU is reduced with 128-thread workgroups; a
-# single-chunk pack of fewer than 4 big (256-thread, 2-step) tiles per CU
+# single-chunk pack of fewer than 4 big (256-thread, 4-step) tiles per CU
 # packs with 128-thread, 1-step tiles.
 KERNEL_SYMBOLS = {
-    "ag_pack": "ag_pack_kernel<1, OneChunk, 256, 2>",
+    "ag_pack": "ag_pack_kernel<1, OneChunk, 256, 4>",
     "ag_unpack": "ag_unpack_kernel<ContigChunks>",
     "rs_pack": "rs_pack_kernel<ContigChunks, 0>",
     "rs_reduce": "rs_reduce_kernel<ContigChunks, unsigned short, 256>",
@@ -72,7 +72,7 @@ SLEEP_CYCLES = 50_000_000                # a device-side wait that lets the host
 # library's choice between the two shapes of each.
 REDUCE_TILE = 256 * 8 * 2
 SMALL_SHARD_TILES_PER_CU = 4
-PACK_BIG_TILE = 256 * 8 * 2
+PACK_BIG_TILE = 256 * 8 * 4
 PACK_BIG_TILES_PER_CU = 4
 
 

@@ -33,7 +33,7 @@ namespace fsdp {
 #define FSDP_PACK_BIG_BLOCK 256
 #endif
 #ifndef FSDP_PACK_BIG_STEPS
-#define FSDP_PACK_BIG_STEPS 2
+#define FSDP_PACK_BIG_STEPS 4
 #endif
 #ifndef FSDP_REDUCE_BLOCK
 #define FSDP_REDUCE_BLOCK 256

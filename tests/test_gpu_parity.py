@@ -161,8 +161,8 @@ def test_grid_stride(case, cap):
 
 @pytest.mark.parametrize("cap", [0, 1, 7, 50])
 @pytest.mark.parametrize("w,dims", [
-    (1, [(4096 * 1100 + 5, 1), (3, 7), (1000, 37)]),
-    (2, [(1000, 4096 * 2 + 8), (5, 3), (7777, 517)]),
+    (1, [(8192 * 1050 + 5, 1), (3, 7), (1000, 37)]),
+    (2, [(2000, 4096 * 2 + 8), (5, 3), (7777, 517)]),
 ])
 def test_pack_big_tiles(w, dims, cap):
     """Buckets large enough for the single-chunk pack's big tiles (at least 4
@@ -171,7 +171,7 @@ def test_pack_big_tiles(w, dims, cap):
     cus = torch.cuda.get_device_properties(DEV).multi_processor_count
     oplan = O.make_plan(w, dims, 8)
     ends = list(oplan.offset[1:]) + [oplan.chunk]
-    big_tiles = sum(-(-(e - o) // 4096) for o, e in zip(oplan.offset, ends))     # 256 threads x 2 x 8
+    big_tiles = sum(-(-(e - o) // 8192) for o, e in zip(oplan.offset, ends))     # 256 threads x 4 x 8
     assert big_tiles >= 4 * cus
     plan = BucketPlan(w, dims, 8, max_workgroups=cap)
     for r in range(w):
