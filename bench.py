@@ -755,17 +755,7 @@ def main(argv=None):
         print(f"bench.py: --rank {rank} is outside 0..{W - 1} for {wl.name}", file=sys.stderr)
         return 2
 
-    # The per-kernel leg under a kernel trace runs first, in a child process,
-    # before this process allocates its own buffers.
     reps = max(1, args.kernel_reps)
-    trace = None
-    if not args.no_trace:
-        child, per, names = traced_child({"mode": "kernels", "workload": args.workload, "rank": rank, "reps": reps,
-                                          "ceilings": args.ceilings})
-        trace = {"error": names} if child is None else {
-            name: {"symbol": names[name], **{"rocprof_" + k: v for k, v in stats_us(per[name][-reps:]).items()}}
-            for name in per}
-
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cus = torch.cuda.get_device_properties(dev).multi_processor_count
@@ -834,9 +824,18 @@ def main(argv=None):
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
-    # ---- the per-kernel leg (after the steps, so that its allocations do not
-    # precede the step buffers): each call over rotating sets of > 1.5 GiB
+    # ---- the per-kernel leg, after the steps (so that neither its allocations
+    # nor its seconds of streaming precede the timed steps): each call over
+    # rotating sets of > 1.5 GiB, here by HIP events and in a child process
+    # under a kernel trace
     leg = kernel_leg(plan, wl, rank, reps, dev, stream)
+    trace = None
+    if not args.no_trace:
+        child, per, names = traced_child({"mode": "kernels", "workload": args.workload, "rank": rank, "reps": reps,
+                                          "ceilings": args.ceilings})
+        trace = {"error": names} if child is None else {
+            name: {"symbol": names[name], **{"rocprof_" + k: v for k, v in stats_us(per[name][-reps:]).items()}}
+            for name in per}
     ceilings = None
     if args.ceilings:
         ceilings = ceiling_leg(plan, rank, reps, dev, stream)
