@@ -50,13 +50,15 @@ KERNELS = ("ag_pack", "ag_unpack", "rs_pack", "rs_reduce")
 # full-size reduce tiles per CU is reduced with 128-thread workgroups; a
 # single-chunk pack of fewer than 4 big (256-thread, 4-step) tiles per CU
 # packs with 128-thread, 1-step tiles.
+# The copies and the reduce have a second form ("true") that the library
+# launches when some segment of the bucket is off the 16-byte grid.
 KERNEL_SYMBOLS = {
     "ag_pack": "ag_pack_kernel<1, OneChunk, 256, 4>",
-    "ag_unpack": "ag_unpack_kernel<ContigChunks>",
-    "rs_pack": "rs_pack_kernel<ContigChunks, 0>",
-    "rs_reduce": "rs_reduce_kernel<ContigChunks, unsigned short, 256>",
+    "ag_unpack": "ag_unpack_kernel<ContigChunks, false>",
+    "rs_pack": "rs_pack_kernel<ContigChunks, 0, false>",
+    "rs_reduce": "rs_reduce_kernel<ContigChunks, unsigned short, 256, false>",
 }
-REDUCE_SMALL_SYMBOL = "rs_reduce_kernel<ContigChunks, unsigned short, 128>"
+REDUCE_SMALL_SYMBOL = "rs_reduce_kernel<ContigChunks, unsigned short, 128, false>"
 PACK_SMALL_SYMBOL = "ag_pack_kernel<1, OneChunk, 128, 1>"
 KERNEL_BASENAMES = ("ag_pack_kernel", "ag_unpack_kernel", "rs_pack_kernel", "rs_reduce_kernel", "probe_read_kernel",
                     "probe_fill_kernel", "probe_copy_kernel", "probe_cast_kernel", "probe_reduce_kernel")
@@ -87,11 +89,16 @@ def algorithmic_bytes(W, S, E, V0):
 
 
 def kernel_symbol(name, plan, rank, cus):
-    """The symbol the call launches for this plan and rank."""
+    """The symbol the call launches for this plan and rank (bf16 wire, one
+    contiguous bucket buffer, 16-byte-aligned tensors)."""
+    P, S = plan.num_params, plan.chunk_elems
+    off_grid = (2 * S) % 16 != 0 or any((2 * plan.offset(p)) % 16 for p in range(P))
+    if name in ("ag_unpack", "rs_pack") and (off_grid or any((2 * plan.seg_elems(p)) % 16 for p in range(P))):
+        return KERNEL_SYMBOLS[name].replace("false>", "true>")
     if name == "rs_reduce":
-        full_tiles = sum(-(-plan.local_elems(p, rank) // REDUCE_TILE) for p in range(plan.num_params))
-        if full_tiles < SMALL_SHARD_TILES_PER_CU * cus:
-            return REDUCE_SMALL_SYMBOL
+        full_tiles = sum(-(-plan.local_elems(p, rank) // REDUCE_TILE) for p in range(P))
+        sym = REDUCE_SMALL_SYMBOL if full_tiles < SMALL_SHARD_TILES_PER_CU * cus else KERNEL_SYMBOLS[name]
+        return sym.replace("false>", "true>") if off_grid else sym
     if name == "ag_pack":
         ends = [plan.offset(p + 1) for p in range(plan.num_params - 1)] + [plan.chunk_elems]
         big = sum(-(-(e - plan.offset(p)) // PACK_BIG_TILE) for p, e in enumerate(ends))
@@ -438,7 +445,7 @@ def child_main(spec_path, out_path):
     out = {"spec": spec}
     if spec["mode"] == "kernels":
         wl = workload(spec["workload"])
-        plan = BucketPlan(wl.world_size, wl.dims)
+        plan = BucketPlan(wl.world_size, wl.dims, spec.get("align", 8))
         out["events"] = kernel_leg(plan, wl, spec["rank"], spec["reps"], dev, stream, labels)
         if spec.get("ceilings"):
             out["ceilings"] = ceiling_leg(plan, spec["rank"], spec["reps"], dev, stream, labels)
@@ -700,6 +707,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3, help="1 toy, 2 8B, 3 70B (default), 4 405B, 5 uneven, 6 70B TP-8 shards, 7 8B at W=128")
     ap.add_argument("--rank", type=int, default=0, help="the rank whose share is timed (0 <= rank < W)")
+    ap.add_argument("--align", type=int, default=8,
+                    help="the plan's alignment A in elements (8: 16-byte segments; 1: the dense concatenation)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip timing the fp32-wire and chunk-table forms after the steps")
@@ -759,7 +768,7 @@ def main(argv=None):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cus = torch.cuda.get_device_properties(dev).multi_processor_count
-    plan = BucketPlan(W, wl.dims)
+    plan = BucketPlan(W, wl.dims, args.align)
     S = plan.chunk_elems
     P = wl.num_params
     E = wl.total_elems
@@ -832,7 +841,7 @@ def main(argv=None):
     trace = None
     if not args.no_trace:
         child, per, names = traced_child({"mode": "kernels", "workload": args.workload, "rank": rank, "reps": reps,
-                                          "ceilings": args.ceilings})
+                                          "ceilings": args.ceilings, "align": args.align})
         trace = {"error": names} if child is None else {
             name: {"symbol": names[name], **{"rocprof_" + k: v for k, v in stats_us(per[name][-reps:]).items()}}
             for name in per}
@@ -877,7 +886,9 @@ def main(argv=None):
 
     copy_ref = None if args.no_variants else time_d2d_copy(gathered, send_buf, stream, args.variant_reps)
 
-    variants = None if args.no_variants else time_variants(
+    # (the chunk-table forms need 16-byte-aligned chunks: a dense bucket with an
+    # odd chunk stride skips them)
+    variants = None if args.no_variants or (2 * S) % 16 else time_variants(
         plan, wl, rank, shards, gathered, params, grads, send_buf, recv, outs, stream, args.variant_reps)
 
     if args.copy_probe:
@@ -907,7 +918,7 @@ def main(argv=None):
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, rank, gpu_plan=plan)
+        cpu = cpu_baseline(wl, rank, gpu_plan=plan, align=args.align)
 
     ms_per_step = elapsed / args.steps * 1e3
     line = {
@@ -924,7 +935,7 @@ def main(argv=None):
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "world_size": W, "rank": rank, "params": P, "chunk_elems": S,
-                   "block_elems": E, "rank_elems": V0, "align_elems": 8, "wire": "bf16",
+                   "block_elems": E, "rank_elems": V0, "align_elems": args.align, "wire": "bf16",
                    "step": "ag_pack+ag_unpack+rs_pack+rs_reduce", "step_bytes": step_bytes},
         "frac_of_peak": round(step_bytes / (elapsed / args.steps) / 1e9 / PEAK_GBPS, 4),
         "kernels": kernels,
@@ -1155,7 +1166,7 @@ def fit_copy_cost(wl, stream, reps=5):
     return res
 
 
-def cpu_baseline(wl, rank=0, min_seconds=10.0, max_passes=50, gpu_plan=None):
+def cpu_baseline(wl, rank=0, min_seconds=10.0, max_passes=50, gpu_plan=None, align=8):
     """The oracle, as it stands, timed on the host: all four steps at ``rank``
     over the whole bucket, repeated until about ``min_seconds`` of CPU work
     has been measured (the oracle is single-threaded numpy).  With
@@ -1169,7 +1180,7 @@ def cpu_baseline(wl, rank=0, min_seconds=10.0, max_passes=50, gpu_plan=None):
 
     dims = list(wl.dims)
     W = wl.world_size
-    plan = O.make_plan(W, dims, 8)
+    plan = O.make_plan(W, dims, align)
     S = plan.chunk
     E = sum(n * k for n, k in dims)
     V0 = sum(O.local_elems(plan, p, rank) for p in range(len(dims)))

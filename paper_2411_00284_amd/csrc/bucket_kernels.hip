@@ -126,6 +126,38 @@ __device__ __forceinline__ uint4 ld16(const void* p) {
 #endif
     return make_uint4(v.x, v.y, v.z, v.w);
 }
+// 16 bytes from an address that is only 2-byte aligned (a segment of a dense
+// bucket, A < 8): the aligned 16-byte block holding p, and when p is not
+// 16-byte aligned the next one too, joined with byte funnel shifts.  Each of
+// the two blocks holds at least one byte of [p, p + 16) and lies inside one
+// 16-byte-aligned block, so it never reaches a page that [p, p + 16) does not.
+__device__ __forceinline__ uint4 ld16_any(const void* p) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    const uint32_t r = uint32_t(a) & 15u;
+    const u32x4* q = reinterpret_cast<const u32x4*>(a - r);
+#if FSDP_NT_LOAD
+    const u32x4 v0 = __builtin_nontemporal_load(q);
+#else
+    const u32x4 v0 = *q;
+#endif
+    if (r == 0) return make_uint4(v0.x, v0.y, v0.z, v0.w);
+#if FSDP_NT_LOAD
+    const u32x4 v1 = __builtin_nontemporal_load(q + 1);
+#else
+    const u32x4 v1 = q[1];
+#endif
+    uint32_t w0, w1, w2, w3, w4;                      // the five words from word r / 4 on
+    switch (r >> 2) {
+        case 0: w0 = v0.x; w1 = v0.y; w2 = v0.z; w3 = v0.w; w4 = v1.x; break;
+        case 1: w0 = v0.y; w1 = v0.z; w2 = v0.w; w3 = v1.x; w4 = v1.y; break;
+        case 2: w0 = v0.z; w1 = v0.w; w2 = v1.x; w3 = v1.y; w4 = v1.z; break;
+        default: w0 = v0.w; w1 = v1.x; w2 = v1.y; w3 = v1.z; w4 = v1.w; break;
+    }
+    const uint32_t b = r & 3u;                         // bytes into word r / 4
+    return make_uint4(__builtin_amdgcn_alignbyte(w1, w0, b), __builtin_amdgcn_alignbyte(w2, w1, b),
+                      __builtin_amdgcn_alignbyte(w3, w2, b), __builtin_amdgcn_alignbyte(w4, w3, b));
+}
+
 // Stores are non-temporal unless kNt is false: a chunk that other workgroups
 // read back at once (the first half of a wide push) is stored through the cache.
 template <bool kNt = bool(FSDP_NT_STORE)>
@@ -202,10 +234,60 @@ struct TableChunks {
 // d[k] = k < v ? s[k] : 0 for k in [lo, hi): one tile of kSteps steps of
 // kCopyBlock threads x 8 elements, in 2-byte units (bf16, or the halves of
 // fp32 words for a plain copy).  `vec`: s and d are 16-byte aligned at 0.
+//
+// When s + lo or d + lo is not 16-byte aligned (a dense bucket, A < 8), the
+// 16-byte stores follow d's alignment grid and each is fed by ld16_any from s;
+// the few elements before d's first and after its last 16-byte unit in the
+// tile are copied one by one (threads 0-7 and 8-15).
 template <int kSteps>
+__device__ __forceinline__ void seg_copy_any(const uint16_t* __restrict__ s, uint16_t* __restrict__ d, int64_t lo,
+                                             int64_t hi, int64_t v) {
+    const int64_t h = (8 - int64_t((reinterpret_cast<uintptr_t>(d + lo) >> 1) & 7)) & 7;
+    const int64_t a = min(lo + h, hi);                 // d + a is 16-byte aligned (or a == hi)
+    const int64_t nv = (hi - a) / kVec;                // whole 16-byte units of d in [a, hi)
+    const int64_t b = a + nv * kVec;
+    const int t = threadIdx.x;
+    if (t < 8) {
+        const int64_t k = lo + t;
+        if (k < a) d[k] = k < v ? s[k] : uint16_t(0);
+    } else if (t < 16) {
+        const int64_t k = b + (t - 8);
+        if (k < hi) d[k] = k < v ? s[k] : uint16_t(0);
+    }
+    uint4 x[kSteps];
+#pragma unroll
+    for (int u = 0; u < kSteps; ++u) {
+        const int64_t g = a + (int64_t(u) * kCopyBlock + t) * kVec;
+        if (g + kVec <= min(v, b)) x[u] = ld16_any(s + g);
+    }
+#pragma unroll
+    for (int u = 0; u < kSteps; ++u) {
+        const int64_t g = a + (int64_t(u) * kCopyBlock + t) * kVec;
+        if (g >= b) continue;
+        if (g + kVec <= v) {
+            st16(d + g, x[u]);
+        } else if (g >= v) {
+            st16(d + g, make_uint4(0, 0, 0, 0));
+        } else {
+            for (int e = 0; e < kVec; ++e) d[g + e] = g + e < v ? s[g + e] : uint16_t(0);
+        }
+    }
+}
+
+// kAny: the launch has segments off the 16-byte grid, which take
+// seg_copy_any; without it such a tile is copied element by element (the
+// host picks kAny only when some segment needs it, so that the aligned
+// kernels keep their own code).
+template <int kSteps, bool kAny>
 __device__ __forceinline__ void seg_copy(const uint16_t* __restrict__ s, uint16_t* __restrict__ d, int64_t lo,
                                          int64_t hi, int64_t v, bool vec) {
     constexpr int64_t kTile = int64_t(kCopyBlock) * kVec * kSteps;
+    if constexpr (kAny) {
+        if (!vec) {
+            seg_copy_any<kSteps>(s, d, lo, hi, v);
+            return;
+        }
+    }
     if (vec && hi - lo == kTile && (hi <= v || lo >= v)) {
         if (hi <= v) {
             uint4 x[kSteps];
@@ -514,7 +596,7 @@ struct UnpackArgs {
     int32_t ntiles;
 };
 
-template <class Chunks>
+template <class Chunks, bool kAny>
 __global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs<Chunks> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
@@ -533,7 +615,7 @@ __global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs<
         if (lo >= hi) continue;
         const uint16_t* s = reinterpret_cast<const uint16_t*>(a.src.at(i)) + a.off[p];
         uint16_t* d = a.dst[p] + int64_t(i) * L;
-        seg_copy<kCopySteps>(s, d, lo, hi, hi, is_aligned16(s) && is_aligned16(d));
+        seg_copy<kCopySteps, kAny>(s, d, lo, hi, hi, is_aligned16(s) && is_aligned16(d));
     }
 }
 
@@ -563,7 +645,7 @@ struct RsPackArgs {
     int32_t ntiles;              // W * tiles_per_dest
 };
 
-template <class Chunks, int kWiden>
+template <class Chunks, int kWiden, bool kAny>
 __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Chunks> a) {
     const int lane = threadIdx.x & 63;
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
@@ -595,7 +677,7 @@ __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Ch
             seg_widen<kCopySteps, kWiden>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
         } else {
             uint16_t* d = reinterpret_cast<uint16_t*>(a.dst.at(j)) + a.off[p];
-            seg_copy<kCopySteps>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
+            seg_copy<kCopySteps, kAny>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
         }
     }
 }
@@ -638,6 +720,7 @@ template <int kB> struct Raw8<uint16_t, kB> {
     uint4 x;
     __device__ __forceinline__ static uint32_t pos(uint32_t t, int e) { return t * 8 + e; }
     __device__ __forceinline__ void load(const uint16_t* row, uint32_t t) { x = ld16(row + t * 8); }
+    __device__ __forceinline__ void load_any(const uint16_t* row, uint32_t t) { x = ld16_any(row + t * 8); }
     __device__ __forceinline__ void init(float (&acc)[8]) const { init8(acc, x); }
     __device__ __forceinline__ void add(float (&acc)[8]) const { add8(acc, x); }
 };
@@ -645,6 +728,7 @@ template <int kB> struct Raw8<_Float16, kB> {
     uint4 x;
     __device__ __forceinline__ static uint32_t pos(uint32_t t, int e) { return t * 8 + e; }
     __device__ __forceinline__ void load(const _Float16* row, uint32_t t) { x = ld16(row + t * 8); }
+    __device__ __forceinline__ void load_any(const _Float16* row, uint32_t t) { x = ld16_any(row + t * 8); }
     __device__ __forceinline__ void init(float (&acc)[8]) const {
         acc[0] = f16_lo(x.x); acc[1] = f16_hi(x.x); acc[2] = f16_lo(x.y); acc[3] = f16_hi(x.y);
         acc[4] = f16_lo(x.z); acc[5] = f16_hi(x.z); acc[6] = f16_lo(x.w); acc[7] = f16_hi(x.w);
@@ -662,6 +746,12 @@ template <int kB> struct Raw8<float, kB> {
     __device__ __forceinline__ void load(const float* row, uint32_t t) {
         a = ld16f(row + t * 4);
         b = ld16f(row + uint32_t(kB) * 4 + t * 4);
+    }
+    __device__ __forceinline__ void load_any(const float* row, uint32_t t) {
+        const uint4 u = ld16_any(row + t * 4);
+        const uint4 w = ld16_any(row + uint32_t(kB) * 4 + t * 4);
+        a = make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w));
+        b = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
     }
     __device__ __forceinline__ void init(float (&acc)[8]) const {
         acc[0] = a.x; acc[1] = a.y; acc[2] = a.z; acc[3] = a.w;
@@ -695,8 +785,9 @@ __device__ __forceinline__ const T* source(const StridedTile<T>& c, int64_t off,
 
 // Loads of sources i0 .. i0+kReduceBatch-1 (those below W unless kFull) of a
 // full tile; all are issued before any of them is used.  `off` is the tile's
-// element offset inside every chunk.
-template <bool kFull, typename T, int kB, class Src>
+// element offset inside every chunk.  kAny: the sources are not 16-byte
+// aligned there (a dense bucket), so each 16 bytes come from ld16_any.
+template <bool kFull, bool kAny, typename T, int kB, class Src>
 __device__ __forceinline__ void load_sources(Raw8<T, kB> (&x)[kReduceBatch][kReduceSteps], const Src& src,
                                              int64_t off, int i0, int W, uint32_t t) {
     constexpr uint32_t kRow = uint32_t(kB) * kVec;
@@ -705,7 +796,10 @@ __device__ __forceinline__ void load_sources(Raw8<T, kB> (&x)[kReduceBatch][kRed
         if (kFull || i0 + b < W) {
             const T* s = source<T>(src, off, i0 + b);
 #pragma unroll
-            for (int u = 0; u < kReduceSteps; ++u) x[b][u].load(s + u * kRow, t);
+            for (int u = 0; u < kReduceSteps; ++u) {
+                if constexpr (kAny) x[b][u].load_any(s + u * kRow, t);
+                else x[b][u].load(s + u * kRow, t);
+            }
         }
     }
 }
@@ -713,15 +807,15 @@ __device__ __forceinline__ void load_sources(Raw8<T, kB> (&x)[kReduceBatch][kRed
 // A full tile of kReduceSteps rows.  The W sources of every output are added
 // in rank order 0..W-1, starting from source 0; the loads of kReduceBatch
 // sources are issued ahead of their adds.
-template <typename T, int kB, class Src>
+template <typename T, int kB, bool kAny, class Src>
 __device__ __forceinline__ void reduce_tile_vec(const Src& src, int64_t off, float* __restrict__ dtile,
                                                 int W, float wf) {
     constexpr uint32_t kRow = uint32_t(kB) * kVec;
     const uint32_t t = threadIdx.x;
     float acc[kReduceSteps][8];
     Raw8<T, kB> x[kReduceBatch][kReduceSteps];
-    if (W >= kReduceBatch) load_sources<true>(x, src, off, 0, W, t);
-    else load_sources<false>(x, src, off, 0, W, t);
+    if (W >= kReduceBatch) load_sources<true, kAny>(x, src, off, 0, W, t);
+    else load_sources<false, kAny>(x, src, off, 0, W, t);
 #pragma unroll
     for (int u = 0; u < kReduceSteps; ++u) x[0][u].init(acc[u]);
 #pragma unroll
@@ -732,14 +826,14 @@ __device__ __forceinline__ void reduce_tile_vec(const Src& src, int64_t off, flo
         }
     int i = kReduceBatch;
     for (; i + kReduceBatch <= W; i += kReduceBatch) {
-        load_sources<true>(x, src, off, i, W, t);
+        load_sources<true, kAny>(x, src, off, i, W, t);
 #pragma unroll
         for (int b = 0; b < kReduceBatch; ++b)
 #pragma unroll
             for (int u = 0; u < kReduceSteps; ++u) x[b][u].add(acc[u]);
     }
     if (i < W) {
-        load_sources<false>(x, src, off, i, W, t);
+        load_sources<false, kAny>(x, src, off, i, W, t);
 #pragma unroll
         for (int b = 0; b < kReduceBatch; ++b)
             if (i + b < W) {
@@ -776,7 +870,7 @@ __device__ __forceinline__ float widen(float x) { return x; }
 // One thread's group of 8 outputs of one row whose group lies wholly inside
 // the shard (partial tiles): the same rank-ordered sum, loads issued
 // kReduceBatch sources ahead.
-template <typename T, int kB, class Src>
+template <typename T, int kB, bool kAny, class Src>
 __device__ __forceinline__ void reduce_group_vec(const Src& src, int64_t off, float* __restrict__ drow, int W,
                                                  float wf, uint32_t t) {
     float acc[8];
@@ -784,7 +878,10 @@ __device__ __forceinline__ void reduce_group_vec(const Src& src, int64_t off, fl
     for (int i = 0; i < W; i += kReduceBatch) {
 #pragma unroll
         for (int b = 0; b < kReduceBatch; ++b)
-            if (i + b < W) x[b].load(source<T>(src, off, i + b), t);
+            if (i + b < W) {
+                if constexpr (kAny) x[b].load_any(source<T>(src, off, i + b), t);
+                else x[b].load(source<T>(src, off, i + b), t);
+            }
 #pragma unroll
         for (int b = 0; b < kReduceBatch; ++b) {
             if (i + b >= W) break;
@@ -815,8 +912,9 @@ __device__ __forceinline__ float reduce_one(const Src& src, int64_t g, int W, fl
 }
 
 // kB threads per workgroup, each owning kReduceSteps groups of 8 outputs: a
-// tile of kB * 8 * kReduceSteps outputs.
-template <class Chunks, typename T, int kB>
+// tile of kB * 8 * kReduceSteps outputs.  kAny: some parameter's sources are
+// off the 16-byte grid (the host picks it only then).
+template <class Chunks, typename T, int kB, bool kAny>
 __global__ void __launch_bounds__(kB) rs_reduce_kernel(const ReduceArgs<Chunks> a) {
     constexpr int64_t kRow = int64_t(kB) * kVec;
     constexpr int64_t kTile = kRow * kReduceSteps;
@@ -832,15 +930,28 @@ __global__ void __launch_bounds__(kB) rs_reduce_kernel(const ReduceArgs<Chunks> 
         const int64_t lo = int64_t(tile - a.tile_start[p]) * kTile;
         const int64_t off = a.off[p];
         float* __restrict__ d0 = a.dst[p];
-        const bool vec = is_aligned16(d0) && a.src.aligned() && ((off * int64_t(sizeof(T))) & 15) == 0;
+        // Outputs are stored 16 bytes at a time when d0 is 16-byte aligned
+        // and the sources loaded 16 bytes at a time: directly when they are
+        // 16-byte aligned, through ld16_any otherwise (kAny only).
+        bool vec, svec;
+        if constexpr (kAny) {
+            vec = is_aligned16(d0);
+            svec = a.src.aligned() && ((off * int64_t(sizeof(T))) & 15) == 0;
+        } else {
+            vec = is_aligned16(d0) && a.src.aligned() && ((off * int64_t(sizeof(T))) & 15) == 0;
+            svec = true;
+        }
         if (vec && lo + kTile <= v) {
             if (std::is_same<Chunks, ContigChunks>::value) {
                 const ContigChunks& c = reinterpret_cast<const ContigChunks&>(a.src);
                 const StridedTile<T> st{reinterpret_cast<const T*>(c.base) + off + lo,
                                         c.stride / int64_t(sizeof(T))};
-                reduce_tile_vec<T, kB>(st, 0, d0 + lo, W, wf);
+                if (!kAny || svec) reduce_tile_vec<T, kB, false>(st, 0, d0 + lo, W, wf);
+                else reduce_tile_vec<T, kB, kAny>(st, 0, d0 + lo, W, wf);
             } else {
-                reduce_tile_vec<T, kB>(reinterpret_cast<const TableChunks&>(a.src), off + lo, d0 + lo, W, wf);
+                const TableChunks& c = reinterpret_cast<const TableChunks&>(a.src);
+                if (!kAny || svec) reduce_tile_vec<T, kB, false>(c, off + lo, d0 + lo, W, wf);
+                else reduce_tile_vec<T, kB, kAny>(c, off + lo, d0 + lo, W, wf);
             }
             continue;
         }
@@ -853,9 +964,12 @@ __global__ void __launch_bounds__(kB) rs_reduce_kernel(const ReduceArgs<Chunks> 
                     const ContigChunks& c = reinterpret_cast<const ContigChunks&>(a.src);
                     const StridedTile<T> st{reinterpret_cast<const T*>(c.base) + off + row,
                                             c.stride / int64_t(sizeof(T))};
-                    reduce_group_vec<T, kB>(st, 0, d0 + row, W, wf, t);
+                    if (!kAny || svec) reduce_group_vec<T, kB, false>(st, 0, d0 + row, W, wf, t);
+                    else reduce_group_vec<T, kB, kAny>(st, 0, d0 + row, W, wf, t);
                 } else {
-                    reduce_group_vec<T, kB>(reinterpret_cast<const TableChunks&>(a.src), off + row, d0 + row, W, wf, t);
+                    const TableChunks& c = reinterpret_cast<const TableChunks&>(a.src);
+                    if (!kAny || svec) reduce_group_vec<T, kB, false>(c, off + row, d0 + row, W, wf, t);
+                    else reduce_group_vec<T, kB, kAny>(c, off + row, d0 + row, W, wf, t);
                 }
                 continue;
             }
@@ -997,6 +1111,13 @@ fsdp_status launch(const Plan& pl, void (*kernel)(const Args), const Args& args,
 
 int64_t tiles(int64_t n, int64_t tile) { return (n + tile - 1) / tile; }
 
+// Whether every chunk of a bucket buffer starts on the 16-byte grid (the host
+// has checked the base and every table entry; a contiguous buffer's stride
+// may still be off the grid in a dense bucket).
+bool chunks_aligned(const ContigChunks& c) { return ((uintptr_t(c.base) | uintptr_t(c.stride)) & 15) == 0; }
+bool chunks_aligned(const TableChunks&) { return true; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
 // ---- ag_pack
 
 // `dst` is the send chunk (OneChunk) or the W destination chunks
@@ -1109,7 +1230,14 @@ fsdp_status do_ag_unpack(const Plan& pl, const Chunks& src, const Spans& ins, in
     a.nparams = pl.nparams;
     a.ntiles = int32_t(nt);
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    return launch(pl, ag_unpack_kernel<Chunks>, a, a.ntiles, kCopyBlock, stream);
+    // Every tile of segment i of parameter p reads chunk i at off_p and writes
+    // params[p] at i * L_p: all on the 16-byte grid unless a stride, offset,
+    // length or pointer is not.
+    bool any = !chunks_aligned(src);
+    for (int p = 0; p < pl.nparams; ++p)
+        if (((a.off[p] * 2) & 15) || ((a.seg[p] * 2) & 15) || !aligned16(a.dst[p])) any = true;
+    if (any) return launch(pl, ag_unpack_kernel<Chunks, true>, a, a.ntiles, kCopyBlock, stream);
+    return launch(pl, ag_unpack_kernel<Chunks, false>, a, a.ntiles, kCopyBlock, stream);
 }
 
 // ---- rs_pack: gradient elements of `gsize` bytes; kWiden (kBF16 / kF16) casts
@@ -1148,7 +1276,16 @@ fsdp_status do_rs_pack(const Plan& pl, const void* const* grads, int gsize, cons
     a.tiles_per_dest = int32_t(nt);
     a.ntiles = int32_t(nt * pl.world);
     if ((st = check_overlap(outs, ins)) != FSDP_OK) return st;
-    return launch(pl, rs_pack_kernel<Chunks, kWiden>, a, a.ntiles, kCopyBlock, stream);
+    // Tiles read grads[p] at j * L_p and write chunk j at off_p (the widening
+    // pack has its own checks and no misaligned vector path).
+    bool any = false;
+    if constexpr (kWiden == kF32) {
+        any = !chunks_aligned(dst);
+        for (int p = 0; p < pl.nparams; ++p)
+            if (((a.off[p] * 2) & 15) || ((a.seg[p] * 2) & 15) || !aligned16(a.src[p])) any = true;
+    }
+    if (any) return launch(pl, rs_pack_kernel<Chunks, kWiden, true>, a, a.ntiles, kCopyBlock, stream);
+    return launch(pl, rs_pack_kernel<Chunks, kWiden, false>, a, a.ntiles, kCopyBlock, stream);
 }
 
 // ---- rs_reduce: received elements of type T
@@ -1206,8 +1343,16 @@ fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const 
     a.world = pl.world;
     a.nparams = pl.nparams;
     a.ntiles = int32_t(nt);
-    if (small) return launch(pl, rs_reduce_kernel<Chunks, T, kReduceBlock / 2>, a, a.ntiles, kReduceBlock / 2, stream);
-    return launch(pl, rs_reduce_kernel<Chunks, T, kReduceBlock>, a, a.ntiles, kReduceBlock, stream);
+    // Sources of parameter p start at off_p in every chunk.
+    bool any = false;
+    for (int p = 0; p < pl.nparams; ++p)
+        if (!chunks_aligned(src) || ((pl.off[p] * int64_t(sizeof(T))) & 15)) any = true;
+    if (small) {
+        if (any) return launch(pl, rs_reduce_kernel<Chunks, T, kReduceBlock / 2, true>, a, a.ntiles, kReduceBlock / 2, stream);
+        return launch(pl, rs_reduce_kernel<Chunks, T, kReduceBlock / 2, false>, a, a.ntiles, kReduceBlock / 2, stream);
+    }
+    if (any) return launch(pl, rs_reduce_kernel<Chunks, T, kReduceBlock, true>, a, a.ntiles, kReduceBlock, stream);
+    return launch(pl, rs_reduce_kernel<Chunks, T, kReduceBlock, false>, a, a.ntiles, kReduceBlock, stream);
 }
 
 }  // namespace

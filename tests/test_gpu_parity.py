@@ -357,6 +357,31 @@ def test_workload_full(key, kernel):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("kernel", ["ag_pack", "ag_unpack", "rs_pack", "rs_reduce"])
+def test_workload_uneven_dense(kernel):
+    """The uneven bucket in the paper-literal dense layout (A = 1): the chunk
+    stride S is odd, so the chunks of odd ranks and every segment after an
+    odd-sized one start off the 16-byte grid (the misaligned vector paths);
+    every output element at full size, ranks 0, W/2 and W-1."""
+    wl = WORKLOADS[5]
+    W = wl.world_size
+    plan = BucketPlan(W, wl.dims, 1)
+    oplan = O.make_plan(W, wl.dims, 1)
+    assert plan.chunk_elems == oplan.chunk and oplan.chunk % 2 == 1
+    if kernel == "ag_pack":
+        for r in _ranks(W):
+            _full_ag_pack(plan, oplan, r, seed=51)
+    elif kernel == "ag_unpack":
+        _full_ag_unpack(plan, oplan, seed=52)
+    elif kernel == "rs_pack":
+        _full_rs_pack(plan, oplan, seed=53)
+    else:
+        for r in _ranks(W):
+            _full_rs_reduce(plan, oplan, r, seed=540 + r)
+    plan.close()
+    torch.cuda.empty_cache()
+
+
 # ----------------------------------------------------------------- the 405B block, in full
 #
 # W = 128, W*S = 3.19e9 elements (64-bit indexing; 6.4 GB per bucket buffer).
