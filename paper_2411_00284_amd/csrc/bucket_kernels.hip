@@ -104,6 +104,22 @@ __device__ __forceinline__ float widen_lo(uint32_t w) { return kFrom == kF16 ? f
 template <int kFrom>
 __device__ __forceinline__ float widen_hi(uint32_t w) { return kFrom == kF16 ? f16_hi(w) : bf16_hi(w); }
 
+#ifndef FSDP_LDS_TABLE
+#define FSDP_LDS_TABLE 0
+#endif
+
+#if FSDP_LDS_TABLE
+// A measured alternative to reading the tile table from the kernel arguments:
+// the first wave stages entries 0..63 (INT_MAX from n on) in LDS, and after a
+// barrier every lane reads its entry there.
+__device__ __forceinline__ int staged_entry(const int32_t* table, int n) {
+    __shared__ int staged[64];
+    if (threadIdx.x < 64) staged[threadIdx.x] = int(threadIdx.x) < n ? table[threadIdx.x] : INT_MAX;
+    __syncthreads();
+    return staged[threadIdx.x & 63];
+}
+#endif
+
 // Parameter owning tile t: the last p with tile_start[p] <= t.  Every lane of
 // the wave holds tile_start[lane] (INT_MAX past the last parameter).
 __device__ __forceinline__ int param_of_tile(int my_start, int t) {
@@ -481,7 +497,11 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
 // tile is kB threads x kS steps of 8 elements.
 template <int kOut, class Dst, int kB, int kS>
 __global__ void __launch_bounds__(kB) ag_pack_kernel(const PackArgs<Dst> a) {
+#if FSDP_LDS_TABLE
+    const int my_start = staged_entry(a.tile_start, PMAX);
+#else
     const int my_start = a.tile_start[threadIdx.x & 63];
+#endif
     int64_t step = blockIdx.x;
     do {
         const int t = int(step);
@@ -497,7 +517,11 @@ __global__ void __launch_bounds__(kB) ag_pack_kernel(const PackArgs<Dst> a) {
 // non-temporal stores streamed at little more than half the rate.)
 template <int kOut>
 __global__ void __launch_bounds__(kPackBlock) push_pack_kernel(const PackArgs<OneChunk> a) {
+#if FSDP_LDS_TABLE
+    const int my_start = staged_entry(a.tile_start, PMAX);
+#else
     const int my_start = a.tile_start[threadIdx.x & 63];
+#endif
     int64_t step = blockIdx.x;
     do {
         const int t = int(step);
@@ -599,7 +623,11 @@ struct UnpackArgs {
 template <class Chunks, bool kAny>
 __global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs<Chunks> a) {
     const int lane = threadIdx.x & 63;
+#if FSDP_LDS_TABLE
+    const int my_start = staged_entry(a.tile_start, a.nparams);
+#else
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
+#endif
     for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
         const int t = int(step);
         const int p = param_of_tile(my_start, t);
@@ -648,7 +676,11 @@ struct RsPackArgs {
 template <class Chunks, int kWiden, bool kAny>
 __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Chunks> a) {
     const int lane = threadIdx.x & 63;
+#if FSDP_LDS_TABLE
+    const int my_start = staged_entry(a.tile_start, a.nparams);
+#else
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
+#endif
     for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
         const int t = int(step);
         int p, j;                                        // parameter, destination rank
@@ -919,7 +951,11 @@ __global__ void __launch_bounds__(kB) rs_reduce_kernel(const ReduceArgs<Chunks> 
     constexpr int64_t kRow = int64_t(kB) * kVec;
     constexpr int64_t kTile = kRow * kReduceSteps;
     const int lane = threadIdx.x & 63;
+#if FSDP_LDS_TABLE
+    const int my_start = staged_entry(a.tile_start, a.nparams);
+#else
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
+#endif
     const int W = a.world;
     const float wf = float(W);
     const uint32_t t = threadIdx.x;
