@@ -252,40 +252,42 @@ struct TableChunks {
 // fp32 words for a plain copy).  `vec`: s and d are 16-byte aligned at 0.
 //
 // When s + lo or d + lo is not 16-byte aligned (a dense bucket, A < 8), the
-// 16-byte stores follow d's alignment grid and each is fed by ld16_any from s;
-// the few elements before d's first and after its last 16-byte unit in the
-// tile are copied one by one (threads 0-7 and 8-15).
+// 16-byte stores follow d's alignment grid and each is fed by ld16_any from s.
+// A tile stores the grid units that start in [lo, hi); its last one may run
+// past hi into the next tile's elements (up to the segment's end e), and the
+// next tile starts at the grid point where it ended, so no 16-byte unit is
+// written in parts by two workgroups.  Only the segment's first elements
+// before the grid (in its first tile) and a last unit cut by e are written
+// element by element.
 template <int kSteps>
 __device__ __forceinline__ void seg_copy_any(const uint16_t* __restrict__ s, uint16_t* __restrict__ d, int64_t lo,
-                                             int64_t hi, int64_t v) {
+                                             int64_t hi, int64_t v, int64_t e) {
     const int64_t h = (8 - int64_t((reinterpret_cast<uintptr_t>(d + lo) >> 1) & 7)) & 7;
-    const int64_t a = min(lo + h, hi);                 // d + a is 16-byte aligned (or a == hi)
-    const int64_t nv = (hi - a) / kVec;                // whole 16-byte units of d in [a, hi)
-    const int64_t b = a + nv * kVec;
+    const int64_t a = lo + h;                          // the first grid point at or after lo
     const int t = threadIdx.x;
-    if (t < 8) {
-        const int64_t k = lo + t;
-        if (k < a) d[k] = k < v ? s[k] : uint16_t(0);
-    } else if (t < 16) {
-        const int64_t k = b + (t - 8);
-        if (k < hi) d[k] = k < v ? s[k] : uint16_t(0);
+    if (lo == 0 && t < 8) {                            // the segment's elements before the grid
+        const int64_t k = t;
+        if (k < min(a, hi)) d[k] = k < v ? s[k] : uint16_t(0);
     }
+    const int64_t nu = hi > a ? (hi - a + kVec - 1) / kVec : 0;   // grid units starting in [a, hi)
     uint4 x[kSteps];
 #pragma unroll
     for (int u = 0; u < kSteps; ++u) {
-        const int64_t g = a + (int64_t(u) * kCopyBlock + t) * kVec;
-        if (g + kVec <= min(v, b)) x[u] = ld16_any(s + g);
+        const int64_t i = int64_t(u) * kCopyBlock + t;
+        const int64_t g = a + i * kVec;
+        if (i < nu && g + kVec <= v && g + kVec <= e) x[u] = ld16_any(s + g);
     }
 #pragma unroll
     for (int u = 0; u < kSteps; ++u) {
-        const int64_t g = a + (int64_t(u) * kCopyBlock + t) * kVec;
-        if (g >= b) continue;
-        if (g + kVec <= v) {
-            st16(d + g, x[u]);
-        } else if (g >= v) {
-            st16(d + g, make_uint4(0, 0, 0, 0));
-        } else {
-            for (int e = 0; e < kVec; ++e) d[g + e] = g + e < v ? s[g + e] : uint16_t(0);
+        const int64_t i = int64_t(u) * kCopyBlock + t;
+        const int64_t g = a + i * kVec;
+        if (i >= nu) continue;
+        if (g + kVec <= e) {
+            if (g + kVec <= v) st16(d + g, x[u]);
+            else if (g >= v) st16(d + g, make_uint4(0, 0, 0, 0));
+            else for (int k = 0; k < kVec; ++k) d[g + k] = g + k < v ? s[g + k] : uint16_t(0);
+        } else {                                       // the segment's last unit, cut by e
+            for (int64_t k = g; k < e; ++k) d[k] = k < v ? s[k] : uint16_t(0);
         }
     }
 }
@@ -294,13 +296,15 @@ __device__ __forceinline__ void seg_copy_any(const uint16_t* __restrict__ s, uin
 // seg_copy_any; without it such a tile is copied element by element (the
 // host picks kAny only when some segment needs it, so that the aligned
 // kernels keep their own code).
+// (vs, e): the segment's valid elements and its end, for seg_copy_any, whose
+// units may run past hi.
 template <int kSteps, bool kAny>
 __device__ __forceinline__ void seg_copy(const uint16_t* __restrict__ s, uint16_t* __restrict__ d, int64_t lo,
-                                         int64_t hi, int64_t v, bool vec) {
+                                         int64_t hi, int64_t v, bool vec, int64_t vs, int64_t e) {
     constexpr int64_t kTile = int64_t(kCopyBlock) * kVec * kSteps;
     if constexpr (kAny) {
         if (!vec) {
-            seg_copy_any<kSteps>(s, d, lo, hi, v);
+            seg_copy_any<kSteps>(s, d, lo, hi, vs, e);
             return;
         }
     }
@@ -643,7 +647,7 @@ __global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs<
         if (lo >= hi) continue;
         const uint16_t* s = reinterpret_cast<const uint16_t*>(a.src.at(i)) + a.off[p];
         uint16_t* d = a.dst[p] + int64_t(i) * L;
-        seg_copy<kCopySteps, kAny>(s, d, lo, hi, hi, is_aligned16(s) && is_aligned16(d));
+        seg_copy<kCopySteps, kAny>(s, d, lo, hi, hi, is_aligned16(s) && is_aligned16(d), v, v);
     }
 }
 
@@ -709,7 +713,7 @@ __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Ch
             seg_widen<kCopySteps, kWiden>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
         } else {
             uint16_t* d = reinterpret_cast<uint16_t*>(a.dst.at(j)) + a.off[p];
-            seg_copy<kCopySteps, kAny>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d));
+            seg_copy<kCopySteps, kAny>(s, d, lo, hi, v, is_aligned16(s) && is_aligned16(d), v, region);
         }
     }
 }
