@@ -356,7 +356,12 @@ def rocprof_path():
                                          else None)
 
 
-def traced_child(spec, timeout=600):
+def progress(msg):
+    """A progress line on stderr (the JSON line alone goes to stdout)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def traced_child(spec, timeout=300):
     spec = dict(spec)
     from paper_2411_00284_amd import _native
     if os.path.abspath(_native.LIB_PATH) != os.path.abspath(os.path.join(ROOT, "paper_2411_00284_amd",
@@ -817,6 +822,7 @@ def main(argv=None):
         if ev is not None:
             ev[4].record(st)
 
+    progress(f"{wl.name}: {args.warmup} warm-up and {args.steps} timed steps")
     for _ in range(args.warmup):
         run_step()
     torch.cuda.synchronize()
@@ -837,9 +843,11 @@ def main(argv=None):
     # nor its seconds of streaming precede the timed steps): each call over
     # rotating sets of > 1.5 GiB, here by HIP events and in a child process
     # under a kernel trace
+    progress("per-kernel leg (HIP events)")
     leg = kernel_leg(plan, wl, rank, reps, dev, stream)
     trace = None
     if not args.no_trace:
+        progress("per-kernel leg under a rocprofv3 kernel trace (child process)")
         child, per, names = traced_child({"mode": "kernels", "workload": args.workload, "rank": rank, "reps": reps,
                                           "ceilings": args.ceilings, "align": args.align})
         trace = {"error": names} if child is None else {
@@ -918,6 +926,7 @@ def main(argv=None):
 
     cpu = None
     if not args.no_cpu_baseline:
+        progress("CPU oracle baseline and full-size parity")
         cpu = cpu_baseline(wl, rank, gpu_plan=plan, align=args.align)
 
     ms_per_step = elapsed / args.steps * 1e3
