@@ -1066,13 +1066,16 @@ constexpr int kMaxSpans = (PMAX > kMaxChunks ? PMAX : kMaxChunks) + 1;
 struct Spans {
     Span s[kMaxSpans];
     int n = 0;
+    bool full = false;   // more spans than kMaxSpans were added (the call is refused)
     void add(const void* p, int64_t bytes) {
         if (n < kMaxSpans) s[n++] = {uintptr_t(p), uintptr_t(p) + uintptr_t(bytes)};
+        else full = true;
     }
 };
 
 // Outputs must be pairwise disjoint and disjoint from every input.
 fsdp_status check_overlap(const Spans& out_spans, const Spans& ins) {
+    if (out_spans.full || ins.full) return fail(FSDP_ERR_TOO_MANY, "too many buffers to check for overlap");
     Spans outs = out_spans;
     Span* const b = outs.s;
     Span* const e = outs.s + outs.n;
