@@ -411,23 +411,71 @@ __device__ __forceinline__ uint2 cast4(float4 a) {
     return make_uint2(cast1<kOut>(a.x) | (cast1<kOut>(a.y) << 16), cast1<kOut>(a.z) | (cast1<kOut>(a.w) << 16));
 }
 
-// Tile lt of parameter p: its part of [off_p, off_{p+1}) of the chunk, the
+// The fields of the parameter a pack tile belongs to.
+struct PackParam {
+    const float* src;
+    int64_t off;       // off_p
+    int64_t region;    // off_{p+1} - off_p
+    int64_t valid;     // n_{p,rank} * inner_p
+};
+
+__device__ __forceinline__ int64_t readlane64(int64_t v, int l) {
+    const uint64_t u = uint64_t(v);
+    const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u)), l));
+    const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u >> 32)), l));
+    return int64_t((uint64_t(hi) << 32) | lo);
+}
+
+// Lane l of every wave holds parameter l's table entries, read from the
+// kernel arguments in one round of independent loads; a tile's parameter
+// fields then come from the owning lane, so a wave's first data load waits
+// on one round trip to the argument table rather than three (the table
+// entry, then off_p, then the shard pointer).
+struct PackLane {
+    int start;          // tile_start[lane]
+    const float* src;
+    int64_t off, end, valid;
+
+    template <class Dst>
+    __device__ __forceinline__ explicit PackLane(const PackArgs<Dst>& a) {
+        const int l = threadIdx.x & 63;
+#if FSDP_LDS_TABLE
+        start = staged_entry(a.tile_start, PMAX);
+#else
+        start = a.tile_start[l];
+#endif
+        src = a.src[l];
+        off = a.off[l];
+        end = a.off[l + 1];
+        valid = a.valid[l];
+    }
+    __device__ __forceinline__ PackParam param(int p) const {
+        const int64_t o = readlane64(off, p);
+        // A shard is device memory: the round trip through the global address
+        // space lets its loads be global rather than flat instructions.
+        typedef const float __attribute__((address_space(1))) GlobalF32;
+        const GlobalF32* g = (const GlobalF32*)(readlane64(reinterpret_cast<int64_t>(src), p));
+        return PackParam{(const float*)g, o, readlane64(end, p) - o, readlane64(valid, p)};
+    }
+};
+
+// Tile lt of parameter pp: its part of [off_p, off_{p+1}) of the chunk, the
 // shard's values cast to bf16 or fp16 or copied as fp32 (kOut), zeros past the shard,
 // written to every destination.  Each thread handles 4 elements per sub-step
 // (16 bytes of fp32 in), so every load and store instruction of a wave covers
 // one contiguous run; the full tiles of a 16-bit push take 8 per thread.
 template <int kOut, class Dst, bool kNt = true, int kB = kPackBlock, int kS = kPackSteps>
-__device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt) {
+__device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, const PackParam& pp, int lt) {
     constexpr int64_t kTile = int64_t(kB) * kVec * kS;
     constexpr bool kCast = kOut != kF32;
     typedef typename std::conditional<kCast, uint16_t, uint32_t>::type Out;
     constexpr int kSub = 2 * kS;
     constexpr bool kOne = std::is_same<Dst, OneChunk>::value;
     const int ndst = kOne ? 1 : a.ndst;
-    const int64_t off = a.off[p];
-    const int64_t region = a.off[p + 1] - off;
-    const int64_t valid = a.valid[p];
-    const float* __restrict__ src = a.src[p];
+    const int64_t off = pp.off;
+    const int64_t region = pp.region;
+    const int64_t valid = pp.valid;
+    const float* __restrict__ src = pp.src;
     const int64_t lo = int64_t(lt) * kTile;
     const int64_t hi = min(lo + kTile, region);
     if (lo >= hi) return;
@@ -496,21 +544,19 @@ __device__ __forceinline__ void pack_tile(const PackArgs<Dst>& a, int p, int lt)
 // wave-ballot lookup.  The pack moves few bytes per launch, so its start-up
 // chain is kept short: tile_start holds INT_MAX past the last parameter (no
 // wait for the parameter count before the table load), the grid never exceeds
-// the tile count (the first tile needs no bound check), and a tile's first
-// index comes from the looked-up lane rather than another table load.  A
-// tile is kB threads x kS steps of 8 elements.
+// the tile count (the first tile needs no bound check), and every field of
+// the tile's parameter comes from the looked-up lane (PackLane), so the only
+// wait before the data loads is the one round of table loads.  The big tile's
+// registers are held to 64 so that 8 waves fit on each SIMD (the extra lane
+// fields had cost one wave).  A tile is kB threads x kS steps of 8 elements.
 template <int kOut, class Dst, int kB, int kS>
-__global__ void __launch_bounds__(kB) ag_pack_kernel(const PackArgs<Dst> a) {
-#if FSDP_LDS_TABLE
-    const int my_start = staged_entry(a.tile_start, PMAX);
-#else
-    const int my_start = a.tile_start[threadIdx.x & 63];
-#endif
+__global__ void __launch_bounds__(kB) __attribute__((amdgpu_waves_per_eu(8))) ag_pack_kernel(const PackArgs<Dst> a) {
+    const PackLane lane(a);
     int64_t step = blockIdx.x;
     do {
         const int t = int(step);
-        const int p = param_of_tile(my_start, t);
-        pack_tile<kOut, Dst, true, kB, kS>(a, p, t - __builtin_amdgcn_readlane(my_start, p));
+        const int p = param_of_tile(lane.start, t);
+        pack_tile<kOut, Dst, true, kB, kS>(a, lane.param(p), t - __builtin_amdgcn_readlane(lane.start, p));
         step += gridDim.x;
     } while (step < a.ntiles);
 }
@@ -521,16 +567,12 @@ __global__ void __launch_bounds__(kB) ag_pack_kernel(const PackArgs<Dst> a) {
 // non-temporal stores streamed at little more than half the rate.)
 template <int kOut>
 __global__ void __launch_bounds__(kPackBlock) push_pack_kernel(const PackArgs<OneChunk> a) {
-#if FSDP_LDS_TABLE
-    const int my_start = staged_entry(a.tile_start, PMAX);
-#else
-    const int my_start = a.tile_start[threadIdx.x & 63];
-#endif
+    const PackLane lane(a);
     int64_t step = blockIdx.x;
     do {
         const int t = int(step);
-        const int p = param_of_tile(my_start, t);
-        pack_tile<kOut, OneChunk, false>(a, p, t - __builtin_amdgcn_readlane(my_start, p));
+        const int p = param_of_tile(lane.start, t);
+        pack_tile<kOut, OneChunk, false>(a, lane.param(p), t - __builtin_amdgcn_readlane(lane.start, p));
         step += gridDim.x;
     } while (step < a.ntiles);
 }
