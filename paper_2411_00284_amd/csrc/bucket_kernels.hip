@@ -419,18 +419,31 @@ struct PackParam {
     int64_t valid;     // n_{p,rank} * inner_p
 };
 
-__device__ __forceinline__ int64_t readlane64(int64_t v, int l) {
+// Lane-held argument tables.  Lane l of a wave loads entry l of each
+// per-parameter table of the kernel arguments, every lane and table in one
+// round of independent loads; from_lane then hands entry p to the whole wave.
+// A kernel that takes its parameter's fields this way waits on one round trip
+// to the argument table before its data loads, not on a chain of them (the
+// tile table, then the entries of the parameter it names).  The pack and the
+// reduce use them.  The copies do not: their tiles are two 16-byte loads per
+// lane, and the tables' extra vector loads per wave made them 3-5 % slower.
+__device__ __forceinline__ int lane_index() { return int(threadIdx.x & 63); }
+__device__ __forceinline__ int32_t from_lane(int32_t v, int p) { return __builtin_amdgcn_readlane(v, p); }
+__device__ __forceinline__ int64_t from_lane(int64_t v, int p) {
     const uint64_t u = uint64_t(v);
-    const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u)), l));
-    const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u >> 32)), l));
+    const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u)), p));
+    const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u >> 32)), p));
     return int64_t((uint64_t(hi) << 32) | lo);
 }
+// A pointer into device memory: the round trip through the global address
+// space keeps its accesses global rather than flat instructions.
+template <typename T>
+__device__ __forceinline__ T* from_lane(T* v, int p) {
+    typedef T __attribute__((address_space(1))) Global;
+    return (T*)(Global*)(from_lane(reinterpret_cast<int64_t>(v), p));
+}
 
-// Lane l of every wave holds parameter l's table entries, read from the
-// kernel arguments in one round of independent loads; a tile's parameter
-// fields then come from the owning lane, so a wave's first data load waits
-// on one round trip to the argument table rather than three (the table
-// entry, then off_p, then the shard pointer).
+// The pack's lane-held table: lane l holds parameter l's entries.
 struct PackLane {
     int start;          // tile_start[lane]
     const float* src;
@@ -438,7 +451,7 @@ struct PackLane {
 
     template <class Dst>
     __device__ __forceinline__ explicit PackLane(const PackArgs<Dst>& a) {
-        const int l = threadIdx.x & 63;
+        const int l = lane_index();
 #if FSDP_LDS_TABLE
         start = staged_entry(a.tile_start, PMAX);
 #else
@@ -450,12 +463,8 @@ struct PackLane {
         valid = a.valid[l];
     }
     __device__ __forceinline__ PackParam param(int p) const {
-        const int64_t o = readlane64(off, p);
-        // A shard is device memory: the round trip through the global address
-        // space lets its loads be global rather than flat instructions.
-        typedef const float __attribute__((address_space(1))) GlobalF32;
-        const GlobalF32* g = (const GlobalF32*)(readlane64(reinterpret_cast<int64_t>(src), p));
-        return PackParam{(const float*)g, o, readlane64(end, p) - o, readlane64(valid, p)};
+        const int64_t o = from_lane(off, p);
+        return PackParam{from_lane(src, p), o, from_lane(end, p) - o, from_lane(valid, p)};
     }
 };
 
@@ -767,7 +776,7 @@ struct ReduceArgs {
     float* dst[PMAX];
     int64_t off[PMAX];
     int64_t valid[PMAX];         // n_{p,rank} * inner_p
-    int32_t tile_start[PMAX];
+    int32_t tile_start[PMAX];    // first tile of parameter p; INT_MAX past the last parameter
     Chunks src;                  // received chunks, one per source rank
     int32_t world;
     int32_t nparams;
@@ -991,27 +1000,30 @@ __device__ __forceinline__ float reduce_one(const Src& src, int64_t g, int W, fl
 
 // kB threads per workgroup, each owning kReduceSteps groups of 8 outputs: a
 // tile of kB * 8 * kReduceSteps outputs.  kAny: some parameter's sources are
-// off the 16-byte grid (the host picks it only then).
+// off the 16-byte grid (the host picks it only then).  The parameter of each
+// tile and its fields come from lane-held tables.
 template <class Chunks, typename T, int kB, bool kAny>
 __global__ void __launch_bounds__(kB) rs_reduce_kernel(const ReduceArgs<Chunks> a) {
     constexpr int64_t kRow = int64_t(kB) * kVec;
     constexpr int64_t kTile = kRow * kReduceSteps;
-    const int lane = threadIdx.x & 63;
+    const int l = lane_index();
 #if FSDP_LDS_TABLE
     const int my_start = staged_entry(a.tile_start, a.nparams);
 #else
-    const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
+    const int my_start = a.tile_start[l];
 #endif
+    const int64_t my_valid = a.valid[l], my_off = a.off[l];
+    float* const my_dst = a.dst[l];
     const int W = a.world;
     const float wf = float(W);
     const uint32_t t = threadIdx.x;
     for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
         const int tile = int(step);
         const int p = param_of_tile(my_start, tile);
-        const int64_t v = a.valid[p];
-        const int64_t lo = int64_t(tile - a.tile_start[p]) * kTile;
-        const int64_t off = a.off[p];
-        float* __restrict__ d0 = a.dst[p];
+        const int64_t v = from_lane(my_valid, p);
+        const int64_t lo = int64_t(tile - from_lane(my_start, p)) * kTile;
+        const int64_t off = from_lane(my_off, p);
+        float* __restrict__ d0 = from_lane(my_dst, p);
         // Outputs are stored 16 bytes at a time when d0 is 16-byte aligned
         // and the sources loaded 16 bytes at a time: directly when they are
         // 16-byte aligned, through ld16_any otherwise (kAny only).
@@ -1424,6 +1436,7 @@ fsdp_status do_rs_reduce(const Plan& pl, int32_t rank, const Chunks& src, const 
         nt += nts[p];
         if (nt > INT32_MAX) return fail(FSDP_ERR_OVERFLOW, "too many work tiles");
     }
+    for (int q = pl.nparams; q < PMAX; ++q) a.tile_start[q] = INT32_MAX;   // never a tile's parameter
     a.src = src;
     a.world = pl.world;
     a.nparams = pl.nparams;
