@@ -61,7 +61,8 @@ KERNEL_SYMBOLS = {
 REDUCE_SMALL_SYMBOL = "rs_reduce_kernel<ContigChunks, unsigned short, 128, false>"
 PACK_SMALL_SYMBOL = "ag_pack_kernel<1, OneChunk, 128, 1>"
 KERNEL_BASENAMES = ("ag_pack_kernel", "ag_unpack_kernel", "rs_pack_kernel", "rs_reduce_kernel", "probe_read_kernel",
-                    "probe_fill_kernel", "probe_copy_kernel", "probe_cast_kernel", "probe_reduce_kernel")
+                    "probe_fill_kernel", "probe_copy_kernel", "probe_cast_kernel", "probe_reduce_kernel",
+                    "probe_empty_kernel")
 PROBES_LIB = os.path.join(ROOT, "paper_2411_00284_amd", "libfsdp_probes.so")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_00284_amd", "csrc", "bucket_kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
@@ -75,6 +76,7 @@ SLEEP_CYCLES = 50_000_000                # a device-side wait that lets the host
 REDUCE_TILE = 256 * 8 * 2
 SMALL_SHARD_TILES_PER_CU = 4
 PACK_BIG_TILE = 256 * 8 * 4
+PACK_SMALL_TILE = 128 * 8
 PACK_BIG_TILES_PER_CU = 4
 
 
@@ -100,9 +102,7 @@ def kernel_symbol(name, plan, rank, cus):
         sym = REDUCE_SMALL_SYMBOL if full_tiles < SMALL_SHARD_TILES_PER_CU * cus else KERNEL_SYMBOLS[name]
         return sym.replace("false>", "true>") if off_grid else sym
     if name == "ag_pack":
-        ends = [plan.offset(p + 1) for p in range(plan.num_params - 1)] + [plan.chunk_elems]
-        big = sum(-(-(e - plan.offset(p)) // PACK_BIG_TILE) for p, e in enumerate(ends))
-        if big < PACK_BIG_TILES_PER_CU * cus:
+        if pack_tiles(plan, PACK_BIG_TILE) < PACK_BIG_TILES_PER_CU * cus:
             return PACK_SMALL_SYMBOL
     return KERNEL_SYMBOLS[name]
 
@@ -253,7 +253,8 @@ def load_probes():
     lib = ctypes.CDLL(PROBES_LIB)
     i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
     sigs = {"probe_read": [vp, i64, vp, vp], "probe_fill": [vp, i64, vp], "probe_copy": [vp, vp, i64, vp],
-            "probe_cast": [vp, vp, i64, vp], "probe_strided_reduce": [vp, i64, i32, vp, i64, i32, vp, vp]}
+            "probe_cast": [vp, vp, i64, vp], "probe_strided_reduce": [vp, i64, i32, vp, i64, i32, vp, vp],
+            "probe_empty": [i64, i32, vp]}
     for name, args in sigs.items():
         fn = getattr(lib, name)
         fn.argtypes = args
@@ -463,6 +464,7 @@ def child_main(spec_path, out_path):
         plan.close()
     elif spec["mode"] == "pack_sweep":
         out["cases"] = pack_sweep_leg(spec["reps"], dev, stream, labels)
+        out["empty"] = empty_launch_leg(spec["reps"], stream, labels)
     out["labels"] = labels
     with open(out_path, "w") as f:
         json.dump(out, f)
@@ -678,6 +680,40 @@ def pack_sweep_leg(reps, dev, stream, labels):
     return res
 
 
+def pack_tiles(plan, tile):
+    """Work tiles of the single-chunk pack with tiles of ``tile`` elements."""
+    ends = [plan.offset(p + 1) for p in range(plan.num_params - 1)] + [plan.chunk_elems]
+    return sum(-(-(e - plan.offset(p)) // tile) for p, e in enumerate(ends))
+
+
+def empty_launch_cases():
+    """Grids that move nothing, for the part of a launch's fixed cost that is
+    dispatch and retirement: one small-tile workgroup, and the 70B block's
+    pack grid (W = 64) in its big and small tiles."""
+    from paper_2411_00284_amd import BucketPlan
+    from synth import workload
+
+    wl = workload(3)
+    plan = BucketPlan(wl.world_size, wl.dims)
+    big, small = pack_tiles(plan, PACK_BIG_TILE), pack_tiles(plan, PACK_SMALL_TILE)
+    plan.close()
+    return [("empty-1x128", 1, 128), (f"empty-{big}x256", big, 256), (f"empty-{small}x128", small, 128)]
+
+
+def empty_launch_leg(reps, stream, labels):
+    lib = load_probes()
+    res = []
+    for name, grid, threads in empty_launch_cases():
+        def call(st, grid=grid, threads=threads):
+            rc = lib.probe_empty(grid, threads, st.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"probe_empty: HIP error {rc}")
+        per, b2b = time_launches([call, call], reps, stream, labels, name, warm=2)
+        res.append({"name": name, "grid": grid, "threads": threads,
+                    **{"event_" + k: v for k, v in stats_us(per).items()}, "b2b_avg_us": round(b2b * 1e3, 3)})
+    return res
+
+
 def pack_sweep(reps):
     """The pack over pack_sweep_cases(), timed by a live kernel trace; fits
     T = t0 + bytes / BW to the trace medians of the block buckets and reports
@@ -699,10 +735,14 @@ def pack_sweep(reps):
     beta, t0 = np.polyfit(x, y, 1)
     r2 = 1.0 - float(np.sum((y - (t0 + beta * x)) ** 2) / np.sum((y - y.mean()) ** 2))
     floor = float(np.median([r["rocprof_median_us"] for r in rows if r["name"].startswith("one-param")]))
+    empty = []
+    for c in child.get("empty", []):
+        st = stats_us(per[c["name"]][-reps:])
+        empty.append({**c, **{"rocprof_" + k: v for k, v in st.items()}})
     return {"kernel": names.get(blocks[0]["name"]), "reps": reps, "cases": rows,
             "fit": {"t0_us": round(float(t0), 3), "GBps": round(1e-3 / float(beta), 1), "r2": round(r2, 5),
                     "points": len(blocks)},
-            "launch_floor_us": round(floor, 3)}
+            "launch_floor_us": round(floor, 3), "empty_launches": empty}
 
 
 def main(argv=None):

@@ -12,6 +12,8 @@
 //   probe_strided_reduce  W strided bf16 sources summed in fp32 in rank order
 //                         and divided by W (the reduce without its parameter
 //                         table), with or without storing the fp32 results
+//   probe_empty           a grid that moves nothing: the fixed cost of
+//                         dispatching and retiring a launch of that shape
 // Accesses are non-temporal, as in the library.  Every launcher checks its
 // sizes and returns a HIP error code; the tiles cover whole 16-byte units
 // (sizes must be multiples of the unit each kernel states).
@@ -160,6 +162,8 @@ __global__ void __launch_bounds__(kRBlock) probe_reduce_kernel(const uint16_t* _
                                         reinterpret_cast<f32x4*>(dst + tile + u * kRow) + h * kRBlock + t);
 }
 
+__global__ void __launch_bounds__(1024) probe_empty_kernel() {}
+
 int64_t blocks(int64_t n, int64_t per) { return (n + per - 1) / per; }
 
 bool grid_ok(int64_t g) { return g >= 0 && g < (int64_t(1) << 31); }
@@ -213,5 +217,12 @@ extern "C" int probe_strided_reduce(const uint16_t* src, int64_t stride, int32_t
         probe_reduce_kernel<true><<<dim3(unsigned(n / kTile)), dim3(kRBlock), 0, stream>>>(src, stride, W, dst, sink);
     else
         probe_reduce_kernel<false><<<dim3(unsigned(n / kTile)), dim3(kRBlock), 0, stream>>>(src, stride, W, dst, sink);
+    return hipGetLastError();
+}
+
+// `grid` workgroups of `threads` threads (1 to 1024) that do nothing.
+extern "C" int probe_empty(int64_t grid, int32_t threads, hipStream_t stream) {
+    if (grid <= 0 || !grid_ok(grid) || threads < 1 || threads > 1024) return hipErrorInvalidValue;
+    probe_empty_kernel<<<dim3(unsigned(grid)), dim3(unsigned(threads)), 0, stream>>>();
     return hipGetLastError();
 }

@@ -79,3 +79,16 @@ def test_pack_sweep_cases_span_the_sizes():
     cases = bench.pack_sweep_cases()
     assert [c.name for c in cases[:3]] == ["one-param-1-tiles", "one-param-64-tiles", "one-param-512-tiles"]
     assert {c.world_size for c in cases[3:]} == {8, 16, 32, 64, 128}
+
+
+def test_empty_launch_grids_are_the_70b_pack_grids():
+    # 13,369,600-element chunk of the 70B block at W = 64 (9 parameters): the
+    # big-tile grid is the pack's 8192-element tile count, the small-tile grid
+    # its 1024-element tile count, and the big one is what the library launches
+    cases = bench.empty_launch_cases()
+    assert cases[0] == ("empty-1x128", 1, 128)
+    (_, big, tb), (_, small, ts) = cases[1], cases[2]
+    assert (tb, ts) == (256, 128)
+    assert 13369600 // 8192 <= big <= 13369600 // 8192 + 9
+    assert 13369600 // 1024 <= small <= 13369600 // 1024 + 9
+    assert big >= bench.PACK_BIG_TILES_PER_CU * 256
