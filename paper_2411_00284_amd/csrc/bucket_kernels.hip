@@ -8,9 +8,10 @@
 // parameter by parameter; the first tile of every parameter is kept in one
 // register per lane of a wavefront, and a ballot over it finds the parameter
 // of any tile in O(1).  The per-parameter table travels in the kernel
-// arguments, read through the scalar cache.  Tile counts fit in 31 bits (the
-// planner checks); grid-stride loops count in 64 bits so that the last step
-// cannot overflow.
+// arguments: the pack and the reduce hold all of it in lanes (lane p holds
+// parameter p's entries), the copies read the looked-up parameter's entries
+// through the scalar cache.  Tile counts fit in 31 bits (the planner checks);
+// grid-stride loops count in 64 bits so that the last step cannot overflow.
 //
 // A bucket buffer of W chunks is addressed either as one allocation (chunk i
 // at base + i*stride) or through a table of W chunk pointers, so the same
@@ -31,12 +32,9 @@
 #include <algorithm>
 #include <atomic>
 #include <climits>
-#include <cstdlib>
 #include <cstdint>
 #include <string>
 #include <type_traits>
-#include <utility>
-#include <vector>
 
 #include "plan_impl.h"
 
@@ -58,6 +56,11 @@ namespace {
 
 constexpr int PMAX = FSDP_MAX_PARAMS;
 constexpr int kMaxChunks = FSDP_MAX_CHUNKS;
+// One parameter per lane of a wave64: the ballot lookup and the lane-held
+// tables need every parameter's entry in one wavefront.
+static_assert(PMAX <= 64, "the tile lookup holds one parameter per lane of a 64-wide wavefront");
+static_assert(kCopyBlock % 64 == 0 && kPackBlock % 64 == 0 && kPackBigBlock % 64 == 0 && kReduceBlock % 128 == 0,
+              "workgroups are whole wavefronts (the reduce's half-size tile included)");
 constexpr int kReduceBatch = FSDP_REDUCE_BATCH;   // source ranks loaded before they are added
 constexpr int kBlocksPerCU = FSDP_BLOCKS_PER_CU;  // workgroups per CU in the grid-stride launch
 
