@@ -47,6 +47,9 @@ namespace {
 #ifndef FSDP_BLOCKS_PER_CU
 #define FSDP_BLOCKS_PER_CU 16384
 #endif
+#ifndef FSDP_XCD_RUN
+#define FSDP_XCD_RUN 256
+#endif
 #ifndef FSDP_NT_LOAD
 #define FSDP_NT_LOAD 1
 #endif
@@ -63,6 +66,9 @@ static_assert(kCopyBlock % 64 == 0 && kPackBlock % 64 == 0 && kPackBigBlock % 64
               "workgroups are whole wavefronts (the reduce's half-size tile included)");
 constexpr int kReduceBatch = FSDP_REDUCE_BATCH;   // source ranks loaded before they are added
 constexpr int kBlocksPerCU = FSDP_BLOCKS_PER_CU;  // workgroups per CU in the grid-stride launch
+constexpr int kXcds = 8;                          // accelerator dies; workgroup b runs on die b % 8
+constexpr int kXcdRun = FSDP_XCD_RUN;             // consecutive copy tiles dealt to one die
+static_assert(kXcdRun >= 1, "a die takes at least one tile at a time");
 
 // ------------------------------------------------------------------ device helpers
 
@@ -604,7 +610,6 @@ __global__ void __launch_bounds__(kPackBlock) push_pack_kernel(const PackArgs<On
 #ifndef FSDP_PUSH_REPLICATE_MIN_W
 #define FSDP_PUSH_REPLICATE_MIN_W 8
 #endif
-constexpr int kXcds = 8;
 constexpr int64_t kRepTile = kCopyBlock;          // 16-byte units per tile (2 KB)
 constexpr int kReplicateMinW = FSDP_PUSH_REPLICATE_MIN_W;
 constexpr int kRepGroupLog2 = 4;
@@ -662,6 +667,24 @@ __global__ void __launch_bounds__(kCopyBlock) replicate_grouped_kernel(const Rep
     }
 }
 
+// ------------------------------------------------------------------ copy tile order
+
+// The copy tile of workgroup-order index b.  Workgroups are dealt to the 8
+// dies (XCDs) round-robin, so in tile order b each die would take every 8th
+// 4 KB tile.  Instead, within each group of 8 * kXcdRun tiles, the workgroups
+// of one die (b, b + 8, b + 16, ...) take kXcdRun consecutive tiles, a 1 MB
+// run per die (1.4 % faster rs_pack and 1 % faster unpack on the 70B block,
+// 1-3 % on the other Llama blocks and the uneven bucket; runs of 16 tiles
+// were 8 % slower, and the reduce gained nothing from such an order); the
+// tiles past the last whole group keep order b.  A bijection
+// on [0, n), so a grid-stride loop over b still covers every tile once.
+__device__ __forceinline__ int copy_tile(int64_t b, int n) {
+    constexpr int64_t kGroup = int64_t(kXcds) * kXcdRun;
+    if (b >= int64_t(n) / kGroup * kGroup) return int(b);
+    const int64_t r = b % kGroup;
+    return int(b - r + (r % kXcds) * kXcdRun + r / kXcds);
+}
+
 // ------------------------------------------------------------------ ag_unpack
 
 // Sizes in 2-byte units (an fp32 element is two units).
@@ -687,7 +710,7 @@ __global__ void __launch_bounds__(kCopyBlock) ag_unpack_kernel(const UnpackArgs<
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
 #endif
     for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
-        const int t = int(step);
+        const int t = copy_tile(step, a.ntiles);
         const int p = param_of_tile(my_start, t);
         const int lt = t - a.tile_start[p];
         const int tps = a.tiles_per_seg[p];
@@ -740,7 +763,7 @@ __global__ void __launch_bounds__(kCopyBlock) rs_pack_kernel(const RsPackArgs<Ch
     const int my_start = lane < a.nparams ? a.tile_start[lane] : INT_MAX;
 #endif
     for (int64_t step = blockIdx.x; step < a.ntiles; step += gridDim.x) {
-        const int t = int(step);
+        const int t = copy_tile(step, a.ntiles);
         int p, j;                                        // parameter, destination rank
         int64_t st;                                      // tile within the segment
         if (a.dest_major) {

@@ -159,6 +159,21 @@ def test_grid_stride(case, cap):
     plan.close()
 
 
+@pytest.mark.parametrize("cap", [0, 1, 7, 300])
+def test_copy_tile_runs(cap):
+    """The copies deal their tiles to the dies in runs (groups of 8 runs,
+    then a tail in plain order); a bucket of two whole groups and a tail,
+    with and without a workgroup cap, copies every element exactly once."""
+    w, dims = 8, [(2_000_000, 5), (4099, 3), (13, 1)]
+    plan = BucketPlan(w, dims, 8, max_workgroups=cap)
+    oplan = O.make_plan(w, dims, 8)
+    tiles = w * sum(-(-L // 2048) for L in oplan.seg)
+    assert 2 * 8 * 256 < tiles < 3 * 8 * 256                  # two whole groups and a tail
+    run_ag_unpack(plan, oplan, seed=cap)
+    run_rs_pack(plan, oplan, seed=cap)
+    plan.close()
+
+
 @pytest.mark.parametrize("cap", [0, 1, 7, 50])
 @pytest.mark.parametrize("w,dims", [
     (1, [(8192 * 1050 + 5, 1), (3, 7), (1000, 37)]),
