@@ -437,6 +437,10 @@ struct PackParam {
 // reduce use them.  The copies do not: their tiles are two 16-byte loads per
 // lane, and the tables' extra vector loads per wave made them 3-5 % slower.
 __device__ __forceinline__ int lane_index() { return int(threadIdx.x & 63); }
+// The table entry a lane loads: its own, or the last one for the lanes past
+// PMAX (none while PMAX is the wavefront width; their tile start is INT_MAX,
+// so the lookup never selects them).
+__device__ __forceinline__ int table_lane() { return min(lane_index(), PMAX - 1); }
 __device__ __forceinline__ int32_t from_lane(int32_t v, int p) { return __builtin_amdgcn_readlane(v, p); }
 __device__ __forceinline__ int64_t from_lane(int64_t v, int p) {
     const uint64_t u = uint64_t(v);
@@ -460,11 +464,11 @@ struct PackLane {
 
     template <class Dst>
     __device__ __forceinline__ explicit PackLane(const PackArgs<Dst>& a) {
-        const int l = lane_index();
+        const int l = table_lane();
 #if FSDP_LDS_TABLE
         start = staged_entry(a.tile_start, PMAX);
 #else
-        start = a.tile_start[l];
+        start = lane_index() < PMAX ? a.tile_start[l] : INT_MAX;
 #endif
         src = a.src[l];
         off = a.off[l];
@@ -1032,11 +1036,11 @@ template <class Chunks, typename T, int kB, bool kAny>
 __global__ void __launch_bounds__(kB) rs_reduce_kernel(const ReduceArgs<Chunks> a) {
     constexpr int64_t kRow = int64_t(kB) * kVec;
     constexpr int64_t kTile = kRow * kReduceSteps;
-    const int l = lane_index();
+    const int l = table_lane();
 #if FSDP_LDS_TABLE
     const int my_start = staged_entry(a.tile_start, a.nparams);
 #else
-    const int my_start = a.tile_start[l];
+    const int my_start = lane_index() < PMAX ? a.tile_start[l] : INT_MAX;
 #endif
     const int64_t my_valid = a.valid[l], my_off = a.off[l];
     float* const my_dst = a.dst[l];
