@@ -433,7 +433,10 @@ struct PackParam {
 // round of independent loads; from_lane then hands entry p to the whole wave.
 // A kernel that takes its parameter's fields this way waits on one round trip
 // to the argument table before its data loads, not on a chain of them (the
-// tile table, then the entries of the parameter it names).  The pack and the
+// tile table, then the entries of the parameter it names).  from_lane is only
+// called where every lane of the wave is active, on values every lane wrote:
+// a lane that is inactive when a value is computed keeps its old register,
+// and readlane would return that.  The pack and the
 // reduce use them.  The copies do not: their tiles are two 16-byte loads per
 // lane, and the tables' extra vector loads per wave made them 3-5 % slower.
 __device__ __forceinline__ int lane_index() { return int(threadIdx.x & 63); }
