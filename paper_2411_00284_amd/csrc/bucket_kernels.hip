@@ -50,6 +50,9 @@ namespace {
 #ifndef FSDP_XCD_RUN
 #define FSDP_XCD_RUN 256
 #endif
+#ifndef FSDP_ANY_NEIGHBOUR
+#define FSDP_ANY_NEIGHBOUR 1
+#endif
 #ifndef FSDP_NT_LOAD
 #define FSDP_NT_LOAD 1
 #endif
@@ -151,26 +154,18 @@ __device__ __forceinline__ uint4 ld16(const void* p) {
 #endif
     return make_uint4(v.x, v.y, v.z, v.w);
 }
-// 16 bytes from an address that is only 2-byte aligned (a segment of a dense
-// bucket, A < 8): the aligned 16-byte block holding p, and when p is not
-// 16-byte aligned the next one too, joined with byte funnel shifts.  Each of
-// the two blocks holds at least one byte of [p, p + 16) and lies inside one
-// 16-byte-aligned block, so it never reaches a page that [p, p + 16) does not.
-__device__ __forceinline__ uint4 ld16_any(const void* p) {
-    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
-    const uint32_t r = uint32_t(a) & 15u;
-    const u32x4* q = reinterpret_cast<const u32x4*>(a - r);
+// One 16-byte-aligned block.
+__device__ __forceinline__ u32x4 ld_block(const u32x4* q) {
 #if FSDP_NT_LOAD
-    const u32x4 v0 = __builtin_nontemporal_load(q);
+    return __builtin_nontemporal_load(q);
 #else
-    const u32x4 v0 = *q;
+    return *q;
 #endif
-    if (r == 0) return make_uint4(v0.x, v0.y, v0.z, v0.w);
-#if FSDP_NT_LOAD
-    const u32x4 v1 = __builtin_nontemporal_load(q + 1);
-#else
-    const u32x4 v1 = q[1];
-#endif
+}
+
+// Bytes [r, r + 16) of the 32 bytes v0 followed by v1 (0 < r < 16), joined
+// with byte funnel shifts.
+__device__ __forceinline__ uint4 join16(const u32x4& v0, const u32x4& v1, uint32_t r) {
     uint32_t w0, w1, w2, w3, w4;                      // the five words from word r / 4 on
     switch (r >> 2) {
         case 0: w0 = v0.x; w1 = v0.y; w2 = v0.z; w3 = v0.w; w4 = v1.x; break;
@@ -181,6 +176,20 @@ __device__ __forceinline__ uint4 ld16_any(const void* p) {
     const uint32_t b = r & 3u;                         // bytes into word r / 4
     return make_uint4(__builtin_amdgcn_alignbyte(w1, w0, b), __builtin_amdgcn_alignbyte(w2, w1, b),
                       __builtin_amdgcn_alignbyte(w3, w2, b), __builtin_amdgcn_alignbyte(w4, w3, b));
+}
+
+// 16 bytes from an address that is only 2-byte aligned (a segment of a dense
+// bucket, A < 8): the aligned 16-byte block holding p, and when p is not
+// 16-byte aligned the next one too, joined with byte funnel shifts.  Each of
+// the two blocks holds at least one byte of [p, p + 16) and lies inside one
+// 16-byte-aligned block, so it never reaches a page that [p, p + 16) does not.
+__device__ __forceinline__ uint4 ld16_any(const void* p) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    const uint32_t r = uint32_t(a) & 15u;
+    const u32x4* q = reinterpret_cast<const u32x4*>(a - r);
+    const u32x4 v0 = ld_block(q);
+    if (r == 0) return make_uint4(v0.x, v0.y, v0.z, v0.w);
+    return join16(v0, ld_block(q + 1), r);
 }
 
 // Stores are non-temporal unless kNt is false: a chunk that other workgroups
@@ -268,6 +277,15 @@ struct TableChunks {
 // written in parts by two workgroups.  Only the segment's first elements
 // before the grid (in its first tile) and a last unit cut by e are written
 // element by element.
+// The block of the next lane (lane l gets lane l + 1's value; lane 63's
+// result is not used): a DPP wave shift, run where every lane is active.
+__device__ __forceinline__ u32x4 next_lane(const u32x4& v) {
+    return u32x4{uint32_t(__builtin_amdgcn_update_dpp(0, int(v.x), 0x130, 0xf, 0xf, false)),
+                 uint32_t(__builtin_amdgcn_update_dpp(0, int(v.y), 0x130, 0xf, 0xf, false)),
+                 uint32_t(__builtin_amdgcn_update_dpp(0, int(v.z), 0x130, 0xf, 0xf, false)),
+                 uint32_t(__builtin_amdgcn_update_dpp(0, int(v.w), 0x130, 0xf, 0xf, false))};
+}
+
 template <int kSteps>
 __device__ __forceinline__ void seg_copy_any(const uint16_t* __restrict__ s, uint16_t* __restrict__ d, int64_t lo,
                                              int64_t hi, int64_t v, int64_t e) {
@@ -280,12 +298,46 @@ __device__ __forceinline__ void seg_copy_any(const uint16_t* __restrict__ s, uin
     }
     const int64_t nu = hi > a ? (hi - a + kVec - 1) / kVec : 0;   // grid units starting in [a, hi)
     uint4 x[kSteps];
+#if FSDP_ANY_NEIGHBOUR
+    // Unit i reads source bytes [s + a + 16 i, + 16): offset r into its aligned
+    // block, the same r for every unit.  For r != 0 it also needs the next
+    // block, which is the block of unit i + 1, loaded by the next lane; that
+    // block is taken from the next lane, so each block is loaded once.  Lane 63
+    // of a wave, and a lane whose next unit is not loaded, load it themselves
+    // (it holds bytes of the unit's own range, as in ld16_any).
+    const uint32_t r = uint32_t(reinterpret_cast<uintptr_t>(s + a)) & 15u;
+    const bool last_lane = (t & 63) == 63;
+    u32x4 b0[kSteps], b1[kSteps];
+    bool ok[kSteps], own[kSteps];
+#pragma unroll
+    for (int u = 0; u < kSteps; ++u) {
+        const int64_t i = int64_t(u) * kCopyBlock + t;
+        const int64_t g = a + i * kVec;
+        ok[u] = i < nu && g + kVec <= v && g + kVec <= e;
+        const bool next_ok = i + 1 < nu && g + 2 * kVec <= v && g + 2 * kVec <= e;
+        own[u] = r != 0 && (last_lane || !next_ok);
+        const u32x4* q = reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(s + g) - r);
+        if (ok[u]) b0[u] = ld_block(q);
+        if (ok[u] && own[u]) b1[u] = ld_block(q + 1);
+    }
+    if (r == 0) {
+#pragma unroll
+        for (int u = 0; u < kSteps; ++u) x[u] = make_uint4(b0[u].x, b0[u].y, b0[u].z, b0[u].w);
+    } else {
+#pragma unroll
+        for (int u = 0; u < kSteps; ++u) {
+            const u32x4 n = next_lane(b0[u]);
+            if (ok[u]) x[u] = join16(b0[u], own[u] ? b1[u] : n, r);
+        }
+    }
+#else
 #pragma unroll
     for (int u = 0; u < kSteps; ++u) {
         const int64_t i = int64_t(u) * kCopyBlock + t;
         const int64_t g = a + i * kVec;
         if (i < nu && g + kVec <= v && g + kVec <= e) x[u] = ld16_any(s + g);
     }
+#endif
 #pragma unroll
     for (int u = 0; u < kSteps; ++u) {
         const int64_t i = int64_t(u) * kCopyBlock + t;
