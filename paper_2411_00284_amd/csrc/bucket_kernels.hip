@@ -265,18 +265,6 @@ struct TableChunks {
 
 // ------------------------------------------------------------------ segment copy
 
-// d[k] = k < v ? s[k] : 0 for k in [lo, hi): one tile of kSteps steps of
-// kCopyBlock threads x 8 elements, in 2-byte units (bf16, or the halves of
-// fp32 words for a plain copy).  `vec`: s and d are 16-byte aligned at 0.
-//
-// When s + lo or d + lo is not 16-byte aligned (a dense bucket, A < 8), the
-// 16-byte stores follow d's alignment grid and each is fed by ld16_any from s.
-// A tile stores the grid units that start in [lo, hi); its last one may run
-// past hi into the next tile's elements (up to the segment's end e), and the
-// next tile starts at the grid point where it ended, so no 16-byte unit is
-// written in parts by two workgroups.  Only the segment's first elements
-// before the grid (in its first tile) and a last unit cut by e are written
-// element by element.
 // The block of the next lane (lane l gets lane l + 1's value; lane 63's
 // result is not used): a DPP wave shift, run where every lane is active.
 __device__ __forceinline__ u32x4 next_lane(const u32x4& v) {
@@ -286,6 +274,19 @@ __device__ __forceinline__ u32x4 next_lane(const u32x4& v) {
                  uint32_t(__builtin_amdgcn_update_dpp(0, int(v.w), 0x130, 0xf, 0xf, false))};
 }
 
+// d[k] = k < v ? s[k] : 0 for k in [lo, hi): one tile of kSteps steps of
+// kCopyBlock threads x 8 elements, in 2-byte units (bf16, or the halves of
+// fp32 words for a plain copy).  `vec`: s and d are 16-byte aligned at 0.
+//
+// When s + lo or d + lo is not 16-byte aligned (a dense bucket, A < 8), the
+// 16-byte stores follow d's alignment grid and each is fed from s with one
+// load per aligned source block (the next lane's block by DPP; see below).
+// A tile stores the grid units that start in [lo, hi); its last one may run
+// past hi into the next tile's elements (up to the segment's end e), and the
+// next tile starts at the grid point where it ended, so no 16-byte unit is
+// written in parts by two workgroups.  Only the segment's first elements
+// before the grid (in its first tile) and a last unit cut by e are written
+// element by element.
 template <int kSteps>
 __device__ __forceinline__ void seg_copy_any(const uint16_t* __restrict__ s, uint16_t* __restrict__ d, int64_t lo,
                                              int64_t hi, int64_t v, int64_t e) {
