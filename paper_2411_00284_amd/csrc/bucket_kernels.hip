@@ -267,11 +267,13 @@ struct TableChunks {
 
 // The block of the next lane (lane l gets lane l + 1's value; lane 63's
 // result is not used): a DPP wave shift, run where every lane is active.
+constexpr int kDppWaveShl1 = 0x130;   // DPP control: each lane reads lane + 1 of the wave
+constexpr int kDppAllRows = 0xf;      // row and bank masks: every row and bank of the wave
+__device__ __forceinline__ uint32_t next_lane(uint32_t v) {
+    return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), kDppWaveShl1, kDppAllRows, kDppAllRows, false));
+}
 __device__ __forceinline__ u32x4 next_lane(const u32x4& v) {
-    return u32x4{uint32_t(__builtin_amdgcn_update_dpp(0, int(v.x), 0x130, 0xf, 0xf, false)),
-                 uint32_t(__builtin_amdgcn_update_dpp(0, int(v.y), 0x130, 0xf, 0xf, false)),
-                 uint32_t(__builtin_amdgcn_update_dpp(0, int(v.z), 0x130, 0xf, 0xf, false)),
-                 uint32_t(__builtin_amdgcn_update_dpp(0, int(v.w), 0x130, 0xf, 0xf, false))};
+    return u32x4{next_lane(v.x), next_lane(v.y), next_lane(v.z), next_lane(v.w)};
 }
 
 // d[k] = k < v ? s[k] : 0 for k in [lo, hi): one tile of kSteps steps of
